@@ -1,0 +1,249 @@
+#!/usr/bin/env python3
+"""Bench of the selective attention-state hot path on one MI355X.
+
+One step = one pass of the whole hot path for one context-parallel rank's
+query block: fresh states of the selected key/value partitions
+(ditango_attn_partition_states), composition with the cached states of the
+others (ditango_merge_states), and contribution weights
+(ditango_contrib).  The state cache is filled from the previous step's
+tensors before timing; all inputs are resident in HBM when timing starts.
+
+Default workload: the video-DiT shape (Wan2.1-14B latent, 75,600 tokens,
+40 heads, head dim 128, 8 partitions of 9,450 tokens, query partition 3,
+fresh partitions {2,3,4}).
+
+Prints one JSON line.  ``value`` is the effective attention throughput of the
+whole step: algorithmic flops of the fresh partitions, 4*B*H*q_len*D*sum(L_j),
+divided by the step time.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "selective-attn step time (ms) + effective TFLOP/s and % bf16 MFMA peak, 1 GPU"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3        # MI355X fp32 MFMA / vector
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="videodit_bf16_h40_d128_s75600_p8")
+    ap.add_argument("--select", default=None, help="comma-separated fresh partitions (default: the workload's)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time of the oracle baseline sample (0 disables it)")
+    ap.add_argument("--no-prefill", action="store_true", help=argparse.SUPPRESS)
+    return ap.parse_args()
+
+
+def algorithmic(w, select):
+    offs = w.offsets
+    q_len = w.q_len
+    keys = sum(offs[j + 1] - offs[j] for j in select)
+    flops = 4.0 * w.B * w.H * q_len * w.D * keys
+    s_state = 2 if w.dtype == "bf16" else 4
+    rows = w.B * w.H * q_len
+    merge_bytes = w.P * rows * (w.D * s_state + 4) + rows * (w.D * s_state + 4)
+    contrib_bytes = (w.P + 1) * rows * 4 + w.P * 4
+    return flops, merge_bytes, contrib_bytes
+
+
+def cpu_baseline(w, x, select, target_s):
+    """The float64 oracle, as it stands, on a bounded sample of query rows of
+    the same step; scaled to the whole step by the row fraction."""
+    import numpy as np
+    import oracle
+    from fixtures import bf16_round
+    offs = w.offsets
+    qa, qb = offs[w.q], offs[w.q + 1]
+    cvt = (lambda a: bf16_round(a).astype(np.float64)) if w.dtype == "bf16" else (lambda a: a.astype(np.float64))
+    K, V = cvt(x["k"]), cvt(x["v"])
+    Kp = cvt(x["k_prev"]) if "k_prev" in x else K
+    Vp = cvt(x["v_prev"]) if "v_prev" in x else V
+    Qall = cvt(x["q"][:, qa:qb])
+    Qp_all = cvt(x["q_prev"][:, qa:qb]) if "q_prev" in x else Qall
+    rng = np.random.default_rng(w.seed + 99)
+
+    def one(n):
+        rows = np.sort(rng.choice(w.q_len, size=n, replace=False))
+        Q = Qall[:, rows]
+        Qp = Qp_all[:, rows]
+        # cached states of the unselected partitions: filled before timing
+        cached = {j: oracle.partition_state(Qp, Kp[:, offs[j]:offs[j + 1]], Vp[:, offs[j]:offs[j + 1]], w.scale)
+                  for j in range(w.P) if j not in select}
+        t0 = time.perf_counter()
+        outs, lses = [], []
+        for j in range(w.P):
+            if j in select:
+                o, l = oracle.partition_state(Q, K[:, offs[j]:offs[j + 1]], V[:, offs[j]:offs[j + 1]], w.scale)
+            else:
+                o, l = cached[j]
+            outs.append(o)
+            lses.append(l)
+        out, lse = oracle.merge(outs, lses)
+        oracle.contrib(lses, lse)
+        return time.perf_counter() - t0
+
+    n0 = min(w.q_len, 32)
+    t0 = one(n0)
+    n = int(min(w.q_len, max(n0, n0 * target_s / max(t0, 1e-3))))
+    t = one(n) if n > n0 else t0
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:   # pragma: no cover
+        cores = 1
+    per_step_s = t * w.q_len / n
+    return n, t, per_step_s, cores
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from fixtures import bf16_bits, gen_qkv, get_workload
+    from paper_2607_15650_amd import api
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+
+    w = get_workload(args.workload)
+    select = tuple(int(s) for s in args.select.split(",")) if args.select else w.select
+    mask = [1 if j in select else 0 for j in range(w.P)]
+    offs = w.offsets
+    qa, qb = offs[w.q], offs[w.q + 1]
+    q_len = w.q_len
+
+    t_gen = time.perf_counter()
+    x = gen_qkv(w, with_prev=True)
+
+    def gpu(a):
+        if w.dtype == "bf16":
+            return torch.from_numpy(bf16_bits(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+
+    q = gpu(np.ascontiguousarray(x["q"][:, qa:qb]))
+    k = gpu(x["k"])
+    v = gpu(x["v"])
+    qp = gpu(np.ascontiguousarray(x["q_prev"][:, qa:qb]))
+    kp = gpu(x["k_prev"])
+    vp = gpu(x["v_prev"])
+    t_gen = time.perf_counter() - t_gen
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+
+    out_states = torch.empty((w.P, w.B, q_len, w.H, w.D), dtype=dt, device="cuda")
+    lse_states = torch.empty((w.P, w.B, w.H, q_len), dtype=torch.float32, device="cuda")
+    out = torch.empty((w.B, q_len, w.H, w.D), dtype=dt, device="cuda")
+    lse = torch.empty((w.B, w.H, q_len), dtype=torch.float32, device="cuda")
+    w_part = torch.empty(w.P, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(16, api.contrib_workspace_bytes(w.B, w.H, q_len, w.P)), dtype=torch.uint8, device="cuda")
+
+    # previous step: every partition's state into the cache (not timed)
+    api.attn_partition_states(qp, kp, vp, offs, [1] * w.P, w.scale, out_states, lse_states)
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        api.attn_partition_states(q, k, v, offs, mask, w.scale, out_states, lse_states)
+        if ev is not None:
+            ev[1].record()
+        api.merge_states(out_states, lse_states, out, lse)
+        if ev is not None:
+            ev[2].record()
+        api.contrib(lse_states, lse, w_part, ws)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] workload {w.name} select {list(select)} warmup {args.warmup} done", file=sys.stderr, flush=True)
+
+    # pass 1: whole-step wall clock (events only at the ends)
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(stop) / args.steps
+
+    # pass 2: per-kernel durations with events between the calls
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t_attn = sorted(e[0].elapsed_time(e[1]) for e in evs)
+    t_merge = sorted(e[1].elapsed_time(e[2]) for e in evs)
+    t_contrib = sorted(e[2].elapsed_time(e[3]) for e in evs)
+    mean = lambda a: sum(a) / len(a)
+    med = lambda a: a[len(a) // 2]
+
+    flops, merge_bytes, contrib_bytes = algorithmic(w, select)
+    attn_ms = mean(t_attn)
+    merge_ms = mean(t_merge)
+    peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    achieved = flops / (attn_ms * 1e-3) / 1e12
+    merge_gbs = merge_bytes / (merge_ms * 1e-3) / 1e9
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
+        n, t, per_step, cores = cpu_baseline(w, x, select, args.cpu_seconds)
+        cpu = {"value": flops / per_step / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+               "sample": f"{n} of {q_len} query rows (all {w.H} heads, all keys of the fresh partitions), "
+                         f"{t:.2f} s; scaled by {q_len}/{n} to {per_step:.1f} s per step"}
+
+    res = {
+        "metric": METRIC,
+        "value": flops / (ms_per_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded N(0,1) plus shared sinusoidal positional component)",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "D": w.D, "S": w.S, "P": w.P,
+                   "query_partition": w.q, "q_len": q_len, "fresh_partitions": list(select),
+                   "fresh_fraction": len(select) / w.P},
+        "roofline": {"bound": "mfma", "kernel": "attn_bf16_kernel" if w.dtype == "bf16" else "attn_f32_kernel",
+                     "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": None},
+        "kernels_ms": {"attn_partition_states": {"mean": attn_ms, "median": med(t_attn)},
+                       "merge_states": {"mean": merge_ms, "median": med(t_merge)},
+                       "contrib": {"mean": mean(t_contrib), "median": med(t_contrib)}},
+        "merge_roofline": {"bound": "hbm", "achieved": merge_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                           "frac": merge_gbs / PEAK_HBM_GBS, "bytes_per_launch": merge_bytes},
+        "attn_tflops_per_step_flops": flops / 1e12,
+        "cpu_baseline": cpu,
+        "input_gen_s": t_gen,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,147 @@
+/*
+ * ditango.h - C ABI of the selective attention-state hot path (gfx950).
+ *
+ * One context-parallel rank's share of one DiT attention call at one
+ * denoising step: the rank's query block attends to P key/value partitions of
+ * the sequence.  Selected partitions get a fresh attention state, the others
+ * keep the state cached at an earlier step, all states are composed, and the
+ * contribution weight of every partition is reported for the next step's
+ * selection (the paper: Sec. 2.2.4, Eq. attention_state and Eq. composition;
+ * Sec. 4.1.2, Eq. lse_weight; Sec. 5.2).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Device pointers point to device memory (HBM) of the current HIP device;
+ *    host pointers (offsets, select, slot lists) are read during the call only.
+ *  - The caller allocates every buffer, the contrib workspace included.  The
+ *    library allocates nothing, frees nothing and never synchronises: kernels
+ *    are enqueued on `stream` (a hipStream_t; NULL = the default stream) and
+ *    run asynchronously.  The library keeps no state between calls and may be
+ *    called from several host threads.
+ *  - Tensors are dense and row-major.  Q is [B][q_len][H][D], K and V are
+ *    [B][S][H][D] (batch, sequence, head, head-dim, the layout in which the
+ *    paper states its workloads).  An attention state of one partition is an
+ *    output OUT [B][q_len][H][D] (normalised, in the state dtype) plus a
+ *    log-sum-exp LSE [B][H][q_len] (float32, natural log, includes `scale`).
+ *    The state cache is a slot array: OUT slots [P][B][q_len][H][D] and LSE
+ *    slots [P][B][H][q_len]; slot j holds partition j's state.
+ *  - bf16 tensors hold IEEE bfloat16 bit patterns (uint16).  Arithmetic is
+ *    float32 (bf16 MFMA products with float32 accumulation for bf16 inputs).
+ *  - Argument errors are detected before anything is launched and return
+ *    DITANGO_ERR_INVALID or DITANGO_ERR_UNSUPPORTED; a failed launch returns
+ *    DITANGO_ERR_HIP.  Nothing is printed and nothing aborts.
+ *  - A partition with no keys has LSE = -inf and OUT = 0 and weight 0.
+ */
+#ifndef DITANGO_H
+#define DITANGO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DITANGO_OK = 0,
+  DITANGO_ERR_INVALID = 1,      /* null pointer, bad size, offsets decreasing, ... */
+  DITANGO_ERR_UNSUPPORTED = 2,  /* valid but not built: head dim, dtype combination */
+  DITANGO_ERR_HIP = 3           /* the HIP runtime reported an error at launch */
+} ditango_status;
+
+typedef enum {
+  DITANGO_F32 = 0,
+  DITANGO_BF16 = 1
+} ditango_dtype;
+
+/* Largest number of partitions (slots) one call accepts. */
+#define DITANGO_MAX_PARTITIONS 64
+
+/*
+ * Fresh attention states of the selected key/value partitions
+ * (Sec. 2.2.4, Eq. attention_state; one call covers every selected partition).
+ *
+ * For every partition j with select[j] != 0, every batch b, head h and query
+ * row r, with keys c in [kv_offsets[j], kv_offsets[j+1]):
+ *     LSE_j[b][h][r] = log sum_c exp(scale * q[b][r][h] . k[b][c][h])
+ *     OUT_j[b][r][h] = sum_c exp(scale * q . k_c - LSE_j) * v[b][c][h]
+ * and writes them to slot j of out_states / lse_states.
+ *
+ *   q, k, v      device; dtype `dt`; Q [B][q_len][H][D], K and V [B][S][H][D]
+ *                with S = kv_offsets[P].
+ *   dt           DITANGO_BF16 or DITANGO_F32 (inputs, states share it).
+ *   D            head dim: 64 or 128.
+ *   kv_offsets   host, P+1 int64, kv_offsets[0] = 0, non-decreasing.
+ *   select       host, P bytes; non-zero = compute partition j fresh.
+ *   scale        softmax scale applied to q.k (normally 1/sqrt(D)).
+ *   out_states   device, [P][B][q_len][H][D] in dtype `dt`.
+ *   lse_states   device, [P][B][H][q_len] float32.
+ *
+ * Slots whose select[j] == 0 are neither read nor written: they keep the state
+ * cached at an earlier step, which is the reuse.  Selecting no partition is
+ * valid and launches nothing.
+ */
+ditango_status ditango_attn_partition_states(
+    const void* q, const void* k, const void* v, ditango_dtype dt,
+    int B, int H, int D, int64_t q_len,
+    const int64_t* kv_offsets, int P, const uint8_t* select, float scale,
+    void* out_states, float* lse_states, void* stream);
+
+/*
+ * Composition of cached and fresh states (Sec. 2.2.4, Eq. composition, n-ary):
+ *     M = max_j LSE_j,  LSE = M + log sum_j exp(LSE_j - M),
+ *     OUT = sum_j exp(LSE_j - LSE) * OUT_j
+ * over the slots listed in `slots` (host, n_slots int32 indices in [0, P));
+ * slots == NULL means all P slots in order.  Rows whose listed LSEs are all
+ * -inf give OUT = 0, LSE = -inf.  Composing a subset into a spare slot is how a
+ * group of states is folded into one cached state.
+ *
+ *   out_states   device, [P][B][q_len][H][D], dtype `state_dt`.
+ *   lse_states   device, [P][B][H][q_len] float32.
+ *   out          device, [B][q_len][H][D], dtype `out_dt`.
+ *   lse_out      device, [B][H][q_len] float32; may be NULL.
+ *   D            head dim: 64 or 128.
+ * The output may not overlap any listed input slot.
+ */
+ditango_status ditango_merge_states(
+    const void* out_states, const float* lse_states, ditango_dtype state_dt,
+    int P, const int32_t* slots, int n_slots,
+    int B, int H, int D, int64_t q_len,
+    void* out, ditango_dtype out_dt, float* lse_out, void* stream);
+
+/*
+ * Bytes of device workspace ditango_contrib needs for these sizes.
+ */
+size_t ditango_contrib_workspace_bytes(int B, int H, int64_t q_len, int P);
+
+/*
+ * Contribution weights of the P partition states to the composed state
+ * (Sec. 4.1.1 w_i, Sec. 4.1.2 Eq. lse_weight):
+ *     W[b][h][r][j] = exp(LSE_j[b][h][r] - LSE[b][h][r])     (0 where LSE = -inf)
+ *     w_part[j]     = mean of W[.][.][.][j] over all B*H*q_len rows.
+ * The row means are reduced in a fixed order, so results are bitwise
+ * identical from run to run.
+ *
+ *   lse_states   device, [P][B][H][q_len] float32.
+ *   lse_out      device, [B][H][q_len] float32 (the composed LSE).
+ *   w_rows       device, [B][H][q_len][P] float32, or NULL to skip.
+ *   w_part       device, [P] float32.
+ *   workspace    device, ditango_contrib_workspace_bytes(...) bytes, 16-byte
+ *                aligned; its contents on entry do not matter.
+ */
+ditango_status ditango_contrib(
+    const float* lse_states, const float* lse_out, int P,
+    int B, int H, int64_t q_len,
+    float* w_rows, float* w_part, void* workspace, void* stream);
+
+/* Static, NUL-terminated description of a status code. */
+const char* ditango_status_string(ditango_status s);
+
+/* Library version as "major.minor.patch". */
+const char* ditango_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DITANGO_H */

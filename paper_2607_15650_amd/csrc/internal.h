@@ -1,0 +1,80 @@
+// internal.h - types and launcher declarations shared by the HIP sources of
+// libditango (not part of the public C ABI; see include/ditango.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "ditango.h"
+
+namespace ditango {
+
+constexpr int kMaxParts = DITANGO_MAX_PARTITIONS;
+
+// One launch of the fresh-state kernel covers every selected partition.
+struct AttnArgs {
+  const void* q;            // [B][q_len][H][D]
+  const void* k;            // [B][S][H][D]
+  const void* v;            // [B][S][H][D]
+  void* out_states;         // [P][B][q_len][H][D]
+  float* lse_states;        // [P][B][H][q_len]
+  int64_t q_len;
+  int64_t S;
+  int B, H;
+  int n_sel;                // number of selected partitions
+  int q_tiles;              // ceil(q_len / rows per workgroup)
+  float scale_log2;         // scale * log2(e): exponents are taken base 2
+  int64_t kv_begin[kMaxParts];
+  int32_t kv_len[kMaxParts];
+  int32_t slot[kMaxParts];
+};
+
+struct MergeArgs {
+  const void* states;       // [P][rows][D]  (rows = B*q_len*H)
+  const float* lse;         // [P][B][H][q_len]
+  void* out;                // [rows][D]
+  float* lse_out;           // [B][H][q_len] or null
+  int64_t q_len;
+  int64_t rows;             // B*q_len*H
+  int B, H;
+  int n;                    // number of listed slots
+  int32_t slots[kMaxParts];
+};
+
+struct ContribArgs {
+  const float* lse;         // [P][n_rows]
+  const float* lse_out;     // [n_rows]
+  float* w_rows;            // [n_rows][P] or null
+  float* w_part;            // [P]
+  float* partial;           // workspace [n_blocks][P]
+  int64_t n_rows;           // B*H*q_len
+  int P;
+  int n_blocks;
+};
+
+// Rows of the composed-LSE array one contrib workgroup reduces.
+constexpr int kContribThreads = 256;
+constexpr int kContribRowsPerThread = 8;
+constexpr int kContribRowsPerBlock = kContribThreads * kContribRowsPerThread;
+
+hipError_t launch_attn_bf16(const AttnArgs& a, int D, hipStream_t s);
+hipError_t launch_attn_f32(const AttnArgs& a, int D, hipStream_t s);
+hipError_t launch_merge(const MergeArgs& a, ditango_dtype sdt, ditango_dtype odt, int D,
+                        hipStream_t s);
+hipError_t launch_contrib(const ContribArgs& a, hipStream_t s);
+
+// Workgroup index remap for the 8 XCDs of the chip: hardware hands out
+// consecutive workgroup ids round-robin over the XCDs, so id b runs on XCD
+// b % 8.  The remap gives every XCD a contiguous run of logical task ids, so
+// tasks that read the same key/value rows (consecutive query tiles of one
+// head and partition) share that XCD's L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+  constexpr int kXcd = 8;
+  const int per = nblocks / kXcd;
+  const int rem = nblocks % kXcd;
+  const int x = bid % kXcd;
+  const int i = bid / kXcd;
+  return x * per + (x < rem ? x : rem) + i;
+}
+
+}  // namespace ditango

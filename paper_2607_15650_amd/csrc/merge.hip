@@ -1,0 +1,200 @@
+// merge.hip - composition of attention states and contribution weights (gfx950).
+//
+// merge: the n-ary state composition of Sec. 2.2.4 (Eq. composition),
+//   M = max_j LSE_j, LSE = M + log sum_j e^{LSE_j - M}, OUT = sum_j e^{LSE_j - LSE} OUT_j,
+// over a list of cached/fresh state slots.  Pure streaming: every OUT slot is
+// read once and the output written once, so the kernel is bound by HBM
+// bandwidth.  Each thread owns 16 bytes of one output row per iteration and
+// issues the loads of all listed slots before using them, so that enough
+// bytes are in flight to cover HBM latency.
+//
+// contrib: per-row weights W_j = e^{LSE_j - LSE} (w_i of Sec. 4.1.1; the
+// anchor weights of Eq. lse_weight) and their mean over all rows per
+// partition, reduced in a fixed order (workgroup tree, then one workgroup over
+// the per-workgroup partial sums) so results are bitwise reproducible.
+#include "internal.h"
+
+namespace ditango {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// 8 consecutive elements of a state row, as float
+template <typename T> struct Vec8;
+template <> struct Vec8<__bf16> {
+  static __device__ __forceinline__ f32x8 load(const __bf16* p) {
+    const bf16x8 x = __builtin_nontemporal_load((const bf16x8*)p);
+    return __builtin_convertvector(x, f32x8);
+  }
+  static __device__ __forceinline__ void store(__bf16* p, const f32x8& v) {
+    *(bf16x8*)p = __builtin_convertvector(v, bf16x8);
+  }
+};
+template <> struct Vec8<float> {
+  static __device__ __forceinline__ f32x8 load(const float* p) {
+    const f32x4 a = __builtin_nontemporal_load((const f32x4*)p);
+    const f32x4 b = __builtin_nontemporal_load((const f32x4*)(p + 4));
+    return f32x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  }
+  static __device__ __forceinline__ void store(float* p, const f32x8& v) {
+    *(f32x4*)p = f32x4{v[0], v[1], v[2], v[3]};
+    *(f32x4*)(p + 4) = f32x4{v[4], v[5], v[6], v[7]};
+  }
+};
+
+constexpr int kMergeThreads = 256;
+constexpr int kMergeUnroll = 8;   // slots loaded per batch
+
+template <typename TS, typename TO, int D>
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a) {
+  constexpr int CPR = D / 8;                      // 8-element chunks per row
+  const int64_t n_chunks = a.rows * CPR;
+  const int64_t slot_elems = a.rows * D;
+  const int64_t lse_slot = (int64_t)a.B * a.H * a.q_len;
+  const TS* __restrict__ st = (const TS*)a.states;
+  TO* __restrict__ out = (TO*)a.out;
+
+  for (int64_t c = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x; c < n_chunks;
+       c += (int64_t)gridDim.x * kMergeThreads) {
+    const int64_t row = c / CPR;                  // row = (b*q_len + r)*H + h
+    const int64_t e0 = c * 8;
+    const int h = (int)(row % a.H);
+    const int64_t br = row / a.H;
+    const int64_t r = br % a.q_len;
+    const int64_t b = br / a.q_len;
+    const int64_t li = (b * a.H + h) * a.q_len + r;
+
+    float mx = -INFINITY;
+    for (int j = 0; j < a.n; ++j) mx = fmaxf(mx, a.lse[(int64_t)a.slots[j] * lse_slot + li]);
+    f32x8 acc = f32x8{};
+    float lse = -INFINITY;
+    if (mx != -INFINITY) {
+      float tot = 0.f;
+      for (int j = 0; j < a.n; ++j)
+        tot += __builtin_amdgcn_exp2f((a.lse[(int64_t)a.slots[j] * lse_slot + li] - mx) * kLog2e);
+      const float inv = 1.0f / tot;
+      lse = mx + __builtin_amdgcn_logf(tot) * kLn2;
+      for (int j0 = 0; j0 < a.n; j0 += kMergeUnroll) {
+        f32x8 x[kMergeUnroll];
+        float w[kMergeUnroll];
+#pragma unroll
+        for (int u = 0; u < kMergeUnroll; ++u) {
+          const int j = j0 + u;
+          if (j < a.n) {
+            const int64_t s = a.slots[j];
+            x[u] = Vec8<TS>::load(st + s * slot_elems + e0);
+            w[u] = __builtin_amdgcn_exp2f((a.lse[s * lse_slot + li] - mx) * kLog2e) * inv;
+          } else {
+            x[u] = f32x8{};
+            w[u] = 0.f;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kMergeUnroll; ++u) acc += w[u] * x[u];
+      }
+    }
+    Vec8<TO>::store(out + e0, acc);
+    if (a.lse_out != nullptr && (c % CPR) == 0) a.lse_out[li] = lse;
+  }
+}
+
+template <typename TS, typename TO, int D>
+hipError_t launch_merge_t(const MergeArgs& a, hipStream_t s) {
+  const int64_t n_chunks = a.rows * (D / 8);
+  if (n_chunks == 0) return hipSuccess;
+  int64_t blocks = (n_chunks + kMergeThreads - 1) / kMergeThreads;
+  const int64_t cap = 256 * 64;   // grid-stride beyond 64 workgroups per CU
+  if (blocks > cap) blocks = cap;
+  hipLaunchKernelGGL((merge_kernel<TS, TO, D>), dim3((unsigned)blocks), dim3(kMergeThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename TS, typename TO>
+hipError_t launch_merge_d(const MergeArgs& a, int D, hipStream_t s) {
+  if (D == 128) return launch_merge_t<TS, TO, 128>(a, s);
+  if (D == 64) return launch_merge_t<TS, TO, 64>(a, s);
+  return hipErrorInvalidValue;
+}
+
+// ---- contribution weights: per-workgroup partial sums, fixed order
+__global__ __launch_bounds__(kContribThreads) void contrib_partial_kernel(const ContribArgs a) {
+  __shared__ float red[kContribThreads];
+  const int tid = threadIdx.x;
+  const int64_t base = (int64_t)blockIdx.x * kContribRowsPerBlock;
+  float lse_row[kContribRowsPerThread];
+#pragma unroll
+  for (int i = 0; i < kContribRowsPerThread; ++i) {
+    const int64_t r = base + i * kContribThreads + tid;
+    lse_row[i] = r < a.n_rows ? a.lse_out[r] : -INFINITY;
+  }
+  for (int j = 0; j < a.P; ++j) {
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < kContribRowsPerThread; ++i) {
+      const int64_t r = base + i * kContribThreads + tid;
+      float w = 0.f;
+      if (r < a.n_rows) {
+        const float lj = a.lse[(int64_t)j * a.n_rows + r];
+        if (lse_row[i] != -INFINITY && lj != -INFINITY)
+          w = __builtin_amdgcn_exp2f((lj - lse_row[i]) * kLog2e);
+        if (a.w_rows != nullptr) a.w_rows[r * a.P + j] = w;
+      }
+      sum += w;
+    }
+    red[tid] = sum;
+    __syncthreads();
+#pragma unroll
+    for (int off = kContribThreads / 2; off > 0; off >>= 1) {
+      if (tid < off) red[tid] += red[tid + off];
+      __syncthreads();
+    }
+    if (tid == 0) a.partial[(int64_t)blockIdx.x * a.P + j] = red[0];
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(kContribThreads) void contrib_final_kernel(const ContribArgs a) {
+  __shared__ float red[kContribThreads];
+  const int tid = threadIdx.x;
+  for (int j = 0; j < a.P; ++j) {
+    float sum = 0.f;
+    for (int blk = tid; blk < a.n_blocks; blk += kContribThreads) sum += a.partial[(int64_t)blk * a.P + j];
+    red[tid] = sum;
+    __syncthreads();
+#pragma unroll
+    for (int off = kContribThreads / 2; off > 0; off >>= 1) {
+      if (tid < off) red[tid] += red[tid + off];
+      __syncthreads();
+    }
+    if (tid == 0) a.w_part[j] = a.n_rows > 0 ? red[0] / (float)a.n_rows : 0.f;
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+hipError_t launch_merge(const MergeArgs& a, ditango_dtype sdt, ditango_dtype odt, int D, hipStream_t s) {
+  if (sdt == DITANGO_BF16 && odt == DITANGO_BF16) return launch_merge_d<__bf16, __bf16>(a, D, s);
+  if (sdt == DITANGO_BF16 && odt == DITANGO_F32) return launch_merge_d<__bf16, float>(a, D, s);
+  if (sdt == DITANGO_F32 && odt == DITANGO_F32) return launch_merge_d<float, float>(a, D, s);
+  if (sdt == DITANGO_F32 && odt == DITANGO_BF16) return launch_merge_d<float, __bf16>(a, D, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_contrib(const ContribArgs& a, hipStream_t s) {
+  if (a.n_blocks > 0) {
+    hipLaunchKernelGGL(contrib_partial_kernel, dim3(a.n_blocks), dim3(kContribThreads), 0, s, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(contrib_final_kernel, dim3(1), dim3(kContribThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace ditango

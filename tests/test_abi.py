@@ -1,0 +1,118 @@
+"""The C-ABI library loads, exports every symbol the header declares, and
+rejects bad arguments with a status code before launching anything.  Runs
+without a GPU: only calls that fail argument validation are made."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ditango.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ditango_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2607_15650_amd import _lib
+    return _lib.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = header_functions()
+    assert "ditango_attn_partition_states" in names and "ditango_merge_states" in names
+    assert "ditango_contrib" in names
+    for n in names:
+        assert hasattr(L, n), n
+    from paper_2607_15650_amd import _lib
+    assert set(names) == set(_lib.SIGNATURES)
+
+
+def test_status_strings_and_version(L):
+    assert L.ditango_status_string(0) == b"ok"
+    assert L.ditango_status_string(1) == b"invalid argument"
+    assert L.ditango_status_string(2) == b"unsupported configuration"
+    assert L.ditango_status_string(3) == b"HIP runtime error"
+    assert re.match(rb"\d+\.\d+\.\d+", L.ditango_version())
+
+
+FAKE = 0x1000  # never dereferenced: every call below fails validation first
+
+
+def attn(L, q=FAKE, k=FAKE, v=FAKE, dt=1, B=1, H=2, D=128, q_len=10, offs=(0, 5, 10),
+         sel=(1, 1), scale=0.1, out=FAKE, lse=FAKE):
+    P = len(offs) - 1 if offs is not None else 1
+    o = (ctypes.c_int64 * len(offs))(*offs) if offs is not None else None
+    s = (ctypes.c_uint8 * len(sel))(*sel) if sel is not None else None
+    return L.ditango_attn_partition_states(q, k, v, dt, B, H, D, q_len, o, P, s,
+                                           scale, out, lse, None)
+
+
+def test_attn_argument_validation(L):
+    assert attn(L, q=None) == 1
+    assert attn(L, out=None) == 1
+    assert attn(L, lse=None) == 1
+    assert attn(L, offs=None) == 1
+    assert attn(L, sel=None) == 1
+    assert attn(L, dt=7) == 1
+    assert attn(L, B=0) == 1
+    assert attn(L, H=0) == 1
+    assert attn(L, q_len=0) == 1
+    assert attn(L, q_len=-3) == 1
+    assert attn(L, D=96) == 2
+    assert attn(L, D=256) == 2
+    assert attn(L, offs=(0, 6, 5), sel=(1, 1)) == 1       # decreasing offsets
+    assert attn(L, offs=(1, 6, 10), sel=(1, 1)) == 1      # offsets[0] != 0
+    assert attn(L, scale=float("nan")) == 1
+    assert attn(L, scale=float("inf")) == 1
+    big = tuple(range(66))
+    assert attn(L, offs=big, sel=(1,) * 65) == 2          # more than 64 partitions
+
+
+def test_attn_empty_selection_launches_nothing(L):
+    # valid arguments, nothing selected: returns OK without touching the GPU
+    assert attn(L, sel=(0, 0)) == 0
+
+
+def merge(L, st=FAKE, lse=FAKE, sdt=1, P=4, slots=None, n=0, B=1, H=2, D=64, q_len=8,
+          out=FAKE, odt=1, lse_out=FAKE):
+    sl = (ctypes.c_int32 * len(slots))(*slots) if slots is not None else None
+    return L.ditango_merge_states(st, lse, sdt, P, sl, n, B, H, D, q_len, out, odt, lse_out, None)
+
+
+def test_merge_argument_validation(L):
+    assert merge(L, st=None) == 1
+    assert merge(L, lse=None) == 1
+    assert merge(L, out=None) == 1
+    assert merge(L, sdt=3) == 1
+    assert merge(L, odt=-1) == 1
+    assert merge(L, P=0) == 1
+    assert merge(L, P=65) == 2
+    assert merge(L, D=32) == 2
+    assert merge(L, q_len=0) == 1
+    assert merge(L, slots=[0, 4], n=2) == 1               # slot out of range
+    assert merge(L, slots=[-1], n=1) == 1
+    assert merge(L, slots=[0], n=0) == 1                  # empty list
+
+
+def test_contrib_argument_validation(L):
+    c = L.ditango_contrib
+    assert c(None, FAKE, 4, 1, 2, 8, None, FAKE, FAKE, None) == 1
+    assert c(FAKE, None, 4, 1, 2, 8, None, FAKE, FAKE, None) == 1
+    assert c(FAKE, FAKE, 4, 1, 2, 8, None, None, FAKE, None) == 1
+    assert c(FAKE, FAKE, 4, 1, 2, 8, None, FAKE, None, None) == 1
+    assert c(FAKE, FAKE, 0, 1, 2, 8, None, FAKE, FAKE, None) == 1
+    assert c(FAKE, FAKE, 65, 1, 2, 8, None, FAKE, FAKE, None) == 2
+    assert c(FAKE, FAKE, 4, 1, 2, 8, None, FAKE, FAKE + 4, None) == 1   # misaligned workspace
+
+
+def test_contrib_workspace_size(L):
+    f = L.ditango_contrib_workspace_bytes
+    assert f(1, 40, 9450, 8) == ((40 * 9450 + 2047) // 2048) * 8 * 4
+    assert f(0, 1, 1, 1) == 0
+    assert f(1, 1, 1, 1) == 4

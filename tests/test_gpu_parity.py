@@ -1,0 +1,328 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle on the
+same seeded inputs.
+
+Tolerances (max-abs, against the oracle evaluated on the exact input values
+the kernels see):
+  bf16 inputs, float32 accumulation: OUT <= 1e-2, LSE <= 2e-3 (V unit variance)
+  float32 inputs:                    OUT <= 1e-5, LSE <= 1e-5
+Selections are given; rankings of the contribution weights must agree exactly
+wherever the oracle's adjacent gap exceeds the weight tolerance.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import fixtures
+import oracle
+from fixtures import gen_qkv, get_workload, sample_rows
+from fixtures.workloads import Workload, partition_offsets
+
+from helpers import TOL, exact_inputs, max_abs, new_state_cache, to_gpu, torch_dtype
+
+pytestmark = pytest.mark.gpu
+
+
+def api():
+    from paper_2607_15650_amd import api as _api
+    return _api
+
+
+def run_step(w, x, select, rows_prev=True):
+    """Populate the cache from the previous step (all partitions), then compute
+    the selected partitions fresh from the current step, merge and contrib.
+    Returns GPU results as numpy."""
+    import torch
+    a = api()
+    offs = w.offsets
+    P = w.P
+    qa, qb = offs[w.q], offs[w.q + 1]
+    q_len = qb - qa
+    dev = {k: to_gpu(v, w.dtype) for k, v in x.items()}
+    out_states, lse_states = new_state_cache(P, w.B, q_len, w.H, w.D, w.dtype)
+    if "q_prev" in dev:
+        a.attn_partition_states(dev["q_prev"][:, qa:qb].contiguous(), dev["k_prev"], dev["v_prev"],
+                                offs, [1] * P, w.scale, out_states, lse_states)
+    a.attn_partition_states(dev["q"][:, qa:qb].contiguous(), dev["k"], dev["v"], offs,
+                            [1 if j in select else 0 for j in range(P)], w.scale, out_states, lse_states)
+    out = torch.empty((w.B, q_len, w.H, w.D), dtype=torch_dtype(w.dtype), device="cuda")
+    lse = torch.empty((w.B, w.H, q_len), dtype=torch.float32, device="cuda")
+    a.merge_states(out_states, lse_states, out, lse)
+    w_part = torch.empty(P, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(16, a.contrib_workspace_bytes(w.B, w.H, q_len, P)), dtype=torch.uint8, device="cuda")
+    w_rows = torch.empty((w.B, w.H, q_len, P), dtype=torch.float32, device="cuda")
+    a.contrib(lse_states, lse, w_part, ws, w_rows)
+    torch.cuda.synchronize()
+    f = lambda t: t.float().cpu().numpy()
+    return dict(out_states=f(out_states), lse_states=f(lse_states), out=f(out), lse=f(lse),
+                w_part=f(w_part), w_rows=f(w_rows))
+
+
+def oracle_step(w, x, select, rows):
+    """Oracle on query rows ``rows`` of the query block (rows are independent)."""
+    offs = w.offsets
+    qa, qb = offs[w.q], offs[w.q + 1]
+    X = {k: exact_inputs(v, w.dtype) for k, v in x.items()}
+    qrow = lambda name: X[name][:, qa:qb][:, rows]
+    sel = [1 if j in select else 0 for j in range(w.P)]
+    if "q_prev" in X:
+        out, lse, outs, lses = oracle.selective_step(
+            qrow("q"), X["k"], X["v"], qrow("q_prev"), X["k_prev"], X["v_prev"], offs, sel, w.scale)
+    else:
+        outs, lses = oracle.partition_states(qrow("q"), X["k"], X["v"], offs, w.scale)
+        out, lse = oracle.merge(outs, lses)
+    W, wbar = oracle.contrib(lses, lse)
+    return dict(outs=outs, lses=lses, out=out, lse=lse, W=W, wbar=wbar)
+
+
+def compare(w, g, o, rows, tol, check_wbar=True):
+    worst = {}
+    for j in range(w.P):
+        e_out = max_abs(g["out_states"][j][:, rows], o["outs"][j])
+        e_lse = max_abs(g["lse_states"][j][:, :, rows], o["lses"][j])
+        worst[f"slot{j}"] = (e_out, e_lse)
+        assert e_out <= tol["out"], (j, e_out)
+        assert e_lse <= tol["lse"], (j, e_lse)
+    e_out = max_abs(g["out"][:, rows], o["out"])
+    e_lse = max_abs(g["lse"][:, :, rows], o["lse"])
+    assert e_out <= tol["out"], ("merged", e_out)
+    assert e_lse <= tol["lse"], ("merged", e_lse)
+    e_w = max_abs(g["w_rows"][:, :, rows], o["W"])
+    assert e_w <= 2 * tol["lse"] + 1e-6, ("w_rows", e_w)
+    if check_wbar:
+        assert max_abs(g["w_part"], o["wbar"]) <= tol["w"]
+        check_ranking(g["w_part"], o["wbar"], w.q, tol["w"])
+    return worst
+
+
+def check_ranking(w_gpu, w_orc, q, tau):
+    """Ranks agree wherever the oracle's adjacent gap exceeds tau."""
+    r_o = oracle.rank_partitions(w_orc, q)
+    r_g = sorted(range(len(w_gpu)), key=lambda j: (-float(w_gpu[j]), abs(j - q), j))
+    vals = [w_orc[j] for j in r_o]
+    # split the oracle ranking into blocks separated by gaps > tau; each block
+    # must hold the same set of partitions in both rankings
+    start = 0
+    for i in range(1, len(r_o) + 1):
+        if i == len(r_o) or vals[i - 1] - vals[i] > tau:
+            assert set(r_o[start:i]) == set(r_g[start:i]), (r_o, r_g)
+            start = i
+
+
+# --------------------------------------------------------------------- workloads
+
+def test_plumbing_f32_all_fresh():
+    w = get_workload("plumbing_f32_h2_d64_s4096_p4")
+    x = gen_qkv(w)
+    g = run_step(w, x, w.select)
+    rows = np.arange(w.q_len)
+    o = oracle_step(w, x, w.select, rows)
+    compare(w, g, o, rows, TOL["f32"])
+    # composing all fresh partitions is full attention
+    X = {k: exact_inputs(v, "f32") for k, v in x.items()}
+    offs = w.offsets
+    fo, fl = oracle.full_attention(X["q"][:, offs[0]:offs[1]], X["k"], X["v"], w.scale)
+    assert max_abs(g["out"], fo) <= 1e-5 and max_abs(g["lse"], fl) <= 1e-5
+
+
+def test_reuse_bf16_all_rows():
+    w = get_workload("reuse_bf16_h12_d64_s16384_p8")
+    x = gen_qkv(w)
+    g = run_step(w, x, w.select)
+    rows = np.arange(w.q_len)
+    o = oracle_step(w, x, w.select, rows)
+    compare(w, g, o, rows, TOL["bf16"])
+
+
+@pytest.mark.slow
+def test_videodit_bf16_sampled_rows():
+    w = get_workload("videodit_bf16_h40_d128_s75600_p8")
+    x = gen_qkv(w)
+    g = run_step(w, x, w.select)
+    rows = sample_rows(w.q_len, 1024, w.seed)
+    o = oracle_step(w, x, w.select, rows)
+    compare(w, g, o, rows, TOL["bf16"])
+
+
+@pytest.mark.slow
+def test_longctx_bf16_sampled_rows_k4():
+    w = get_workload("longctx_bf16_h24_d128_s131072_p16")
+    x = gen_qkv(w)
+    g = run_step(w, x, w.select)
+    rows = sample_rows(w.q_len, 384, w.seed)
+    o = oracle_step(w, x, w.select, rows)
+    compare(w, g, o, rows, TOL["bf16"])
+
+
+# --------------------------------------------------------------------- ragged / edge shapes
+
+EDGE = [
+    # (dtype, D, H, q_len, partition lengths)
+    ("bf16", 128, 3, 300, [0, 1, 63, 65, 200]),
+    ("bf16", 64, 2, 1, [7, 64, 129]),
+    ("bf16", 128, 1, 257, [256, 255, 1]),
+    ("bf16", 64, 5, 513, [100, 0, 333]),
+    ("f32", 128, 2, 129, [31, 33, 96]),
+    ("f32", 64, 3, 40, [0, 5, 70]),
+]
+
+
+@pytest.mark.parametrize("dtype,D,H,q_len,lens", EDGE)
+def test_ragged_shapes(dtype, D, H, q_len, lens):
+    import torch
+    a = api()
+    rng = np.random.default_rng(q_len * 7 + D)
+    B = 2 if q_len < 100 else 1
+    S = sum(lens)
+    offs = [0]
+    for n in lens:
+        offs.append(offs[-1] + n)
+    P = len(lens)
+    q = rng.standard_normal((B, q_len, H, D), dtype=np.float32)
+    k = rng.standard_normal((B, S, H, D), dtype=np.float32) + 0.3
+    v = rng.standard_normal((B, S, H, D), dtype=np.float32)
+    scale = 1 / math.sqrt(D)
+    out_states, lse_states = new_state_cache(P, B, q_len, H, D, dtype)
+    a.attn_partition_states(to_gpu(q, dtype), to_gpu(k, dtype), to_gpu(v, dtype), offs, [1] * P, scale,
+                            out_states, lse_states)
+    out = torch.empty((B, q_len, H, D), dtype=torch_dtype(dtype), device="cuda")
+    lse = torch.empty((B, H, q_len), dtype=torch.float32, device="cuda")
+    a.merge_states(out_states, lse_states, out, lse)
+    torch.cuda.synchronize()
+    Q, K, V = (exact_inputs(t, dtype) for t in (q, k, v))
+    outs, lses = oracle.partition_states(Q, K, V, offs, scale)
+    tol = TOL[dtype]
+    for j in range(P):
+        gl = lse_states[j].cpu().numpy()
+        go = out_states[j].float().cpu().numpy()
+        if lens[j] == 0:
+            assert np.all(np.isneginf(gl)) and np.all(go == 0)
+        assert max_abs(go, outs[j]) <= tol["out"], j
+        assert max_abs(gl, lses[j]) <= tol["lse"], j
+    mo, ml = oracle.merge(outs, lses)
+    assert max_abs(out.float().cpu().numpy(), mo) <= tol["out"]
+    assert max_abs(lse.cpu().numpy(), ml) <= tol["lse"]
+
+
+def test_unselected_slots_untouched_bitwise():
+    import torch
+    a = api()
+    w = Workload(name="t", dtype="bf16", B=1, H=3, D=128, grid=(4, 16, 16), P=8, q=3, seed=9, select=(2, 3, 4))
+    x = gen_qkv(w, with_prev=False)
+    offs = w.offsets
+    qa, qb = offs[w.q], offs[w.q + 1]
+    out_states, lse_states = new_state_cache(w.P, w.B, w.q_len, w.H, w.D, "bf16", fill=0x5A5A)
+    before_o = out_states.clone()
+    before_l = lse_states.clone()
+    a.attn_partition_states(to_gpu(x["q"][:, qa:qb], "bf16"), to_gpu(x["k"], "bf16"), to_gpu(x["v"], "bf16"),
+                            offs, w.select_mask(), w.scale, out_states, lse_states)
+    torch.cuda.synchronize()
+    for j in range(w.P):
+        same_o = torch.equal(out_states[j].view(torch.int16), before_o[j].view(torch.int16))
+        same_l = torch.equal(lse_states[j].view(torch.int32), before_l[j].view(torch.int32))
+        assert same_o == same_l == (j not in w.select), j
+
+
+def test_determinism_and_reuse_with_unchanged_cache_bitwise():
+    import torch
+    a = api()
+    w = Workload(name="t", dtype="bf16", B=1, H=4, D=128, grid=(8, 16, 16), P=8, q=3, seed=10, select=(2, 3, 4))
+    x = gen_qkv(w, with_prev=False)
+    offs = w.offsets
+    qa, qb = offs[w.q], offs[w.q + 1]
+    q, k, v = (to_gpu(t, "bf16") for t in (x["q"][:, qa:qb], x["k"], x["v"]))
+
+    def full():
+        os_, ls_ = new_state_cache(w.P, w.B, w.q_len, w.H, w.D, "bf16")
+        a.attn_partition_states(q, k, v, offs, [1] * w.P, w.scale, os_, ls_)
+        return os_, ls_
+
+    o1, l1 = full()
+    o2, l2 = full()
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+    # reuse with an unchanged cache: recompute only the selection over a cache
+    # computed from the same tensors -> bitwise equal to all fresh
+    o3, l3 = o1.clone(), l1.clone()
+    a.attn_partition_states(q, k, v, offs, w.select_mask(), w.scale, o3, l3)
+    outs = []
+    for os_, ls_ in ((o1, l1), (o3, l3)):
+        out = torch.empty((w.B, w.q_len, w.H, w.D), dtype=torch.float32, device="cuda")
+        lse = torch.empty((w.B, w.H, w.q_len), dtype=torch.float32, device="cuda")
+        a.merge_states(os_, ls_, out, lse)
+        outs.append((out, lse))
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+    # slot order only changes rounding of the float32 composition
+    perm = [5, 2, 7, 0, 3, 6, 1, 4]
+    out_p = torch.empty_like(outs[0][0])
+    lse_p = torch.empty_like(outs[0][1])
+    a.merge_states(o1, l1, out_p, lse_p, slots=perm)
+    torch.cuda.synchronize()
+    assert (out_p - outs[0][0]).abs().max().item() <= 1e-6
+    assert (lse_p - outs[0][1]).abs().max().item() <= 1e-6
+    # contrib is bitwise reproducible
+    wp = []
+    for _ in range(2):
+        w_part = torch.empty(w.P, dtype=torch.float32, device="cuda")
+        ws = torch.empty(a.contrib_workspace_bytes(w.B, w.H, w.q_len, w.P), dtype=torch.uint8, device="cuda")
+        a.contrib(l1, outs[0][1], w_part, ws)
+        wp.append(w_part)
+    torch.cuda.synchronize()
+    assert torch.equal(wp[0], wp[1])
+
+
+# --------------------------------------------------------------------- merge / contrib in isolation
+
+@pytest.mark.parametrize("state_dt,out_dt,D", [("bf16", "bf16", 128), ("bf16", "f32", 64), ("f32", "f32", 128)])
+def test_merge_kernel_on_oracle_states(state_dt, out_dt, D):
+    """Merge of given states (including -inf rows and a subset slot list)
+    against the oracle's composition of the same stored values."""
+    import torch
+    a = api()
+    rng = np.random.default_rng(D)
+    P, B, q_len, H = 6, 2, 77, 3
+    outs = rng.standard_normal((P, B, q_len, H, D)).astype(np.float32)
+    lses = (rng.standard_normal((P, B, H, q_len)) * 3).astype(np.float32)
+    lses[1, 0, 1, :10] = -np.inf                   # one partition empty for some rows
+    lses[:, 1, 2, 5] = -np.inf                     # one row with every partition empty
+    slots = [4, 0, 1, 5, 2]
+    st = to_gpu(outs, state_dt)
+    ls = torch.from_numpy(lses).cuda()
+    out = torch.empty((B, q_len, H, D), dtype=torch_dtype(out_dt), device="cuda")
+    lse = torch.empty((B, H, q_len), dtype=torch.float32, device="cuda")
+    a.merge_states(st.contiguous(), ls, out, lse, slots=slots)
+    torch.cuda.synchronize()
+    O = exact_inputs(outs, state_dt)
+    mo, ml = oracle.merge([O[j] for j in slots], [lses[j].astype(np.float64) for j in slots])
+    go = out.float().cpu().numpy()
+    gl = lse.cpu().numpy()
+    assert not np.isnan(go).any() and not np.isnan(gl).any()
+    assert np.all(go[1, 5, 2] == 0) and np.isneginf(gl[1, 2, 5])
+    # float32 output: float32 arithmetic; bf16 output: plus one bf16 rounding
+    tol_out = 1e-5 if out_dt == "f32" else float(np.abs(mo).max()) * 2.0 ** -8 + 1e-6
+    assert max_abs(go, mo) <= tol_out
+    assert max_abs(gl, ml) <= 5e-6
+
+
+def test_contrib_kernel_against_oracle():
+    import torch
+    a = api()
+    rng = np.random.default_rng(3)
+    P, B, H, q_len = 8, 1, 7, 3001
+    lses = (rng.standard_normal((P, B, H, q_len)) * 2).astype(np.float32)
+    lses[3] -= 4.0
+    lses[0, 0, 0, :100] = -np.inf
+    mo, ml = oracle.merge([np.zeros((B, q_len, H, 1))] * P, [l.astype(np.float64) for l in lses])
+    ml32 = ml.astype(np.float32)
+    W, wbar = oracle.contrib([l.astype(np.float64) for l in lses], ml32.astype(np.float64))
+    ls = torch.from_numpy(lses).cuda()
+    lo = torch.from_numpy(ml32).cuda()
+    w_part = torch.empty(P, dtype=torch.float32, device="cuda")
+    w_rows = torch.empty((B, H, q_len, P), dtype=torch.float32, device="cuda")
+    ws = torch.empty(a.contrib_workspace_bytes(B, H, q_len, P), dtype=torch.uint8, device="cuda")
+    a.contrib(ls, lo, w_part, ws, w_rows)
+    torch.cuda.synchronize()
+    assert max_abs(w_rows.cpu().numpy(), W) <= 1e-6
+    assert max_abs(w_part.cpu().numpy(), wbar) <= 1e-6
+    check_ranking(w_part.cpu().numpy(), wbar, 3, 1e-6)
