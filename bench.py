@@ -43,7 +43,9 @@ def parse():
     ap.add_argument("--select", default=None, help="comma-separated fresh partitions (default: the workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
-    ap.add_argument("--no-prefill", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="before timing, run one plain elementwise copy of this many MiB "
+                         "(the reference kernel that scales profiler byte counters)")
     return ap.parse_args()
 
 
@@ -154,6 +156,14 @@ def main():
     lse = torch.empty((w.B, w.H, q_len), dtype=torch.float32, device="cuda")
     w_part = torch.empty(w.P, dtype=torch.float32, device="cuda")
     ws = torch.empty(max(16, api.contrib_workspace_bytes(w.B, w.H, q_len, w.P)), dtype=torch.uint8, device="cuda")
+
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     # previous step: every partition's state into the cache (not timed)
     api.attn_partition_states(qp, kp, vp, offs, [1] * w.P, w.scale, out_states, lse_states)
