@@ -47,8 +47,9 @@ def _compile(src: str, obj: str, extra) -> None:
         raise RuntimeError(f"hipcc failed on {os.path.basename(src)}:\n{r.stderr}")
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    objdir = os.path.join(HERE, "_build")
+def build(verbose: bool = False, extra=(), out: str = LIB, objdir: str = "") -> str:
+    """Compile every source and link ``out``; ``extra`` flags go to each compile."""
+    objdir = objdir or os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
     jobs = []
     with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES), 8)) as ex:
@@ -57,15 +58,15 @@ def build(verbose: bool = False, extra=()) -> str:
             jobs.append((obj, ex.submit(_compile, os.path.join(CSRC, s), obj, extra)))
         for _, f in jobs:
             f.result()
-    tmp = LIB + ".tmp"
+    tmp = out + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + [o for o, _ in jobs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {out}")
+    return out
 
 
 if __name__ == "__main__":

@@ -9,22 +9,38 @@
 //
 // Work decomposition
 //   One workgroup = NW waves = one tile of NW*QB*32 query rows of one
-//   (batch, head, selected partition).  Each wave owns QB blocks of 32 query
-//   rows.  The workgroup walks the partition's keys in tiles of BN keys; K and
-//   V tiles are staged through LDS (double buffered: the global loads of tile
-//   i+1 are in flight while tile i is computed) and shared by all waves.
+//   (batch, head, selected partition); a single launch covers every selected
+//   partition.  Each wave owns QB blocks of 32 query rows.  The workgroup walks
+//   the partition's keys in tiles of BN keys.  K and V tiles go straight from
+//   global memory into LDS with the 16-byte direct loads (no staging
+//   registers, no LDS write instructions), double buffered, and are shared by
+//   all waves of the workgroup.
 //
 // Orientation
 //   Scores are computed transposed, S^T = K Q^T, with the 32x32x16 bf16 MFMA:
-//   A = K (32 keys x 16 dims, read from LDS), B = Q^T (16 dims x 32 queries,
-//   held in registers for the whole kernel).  In the 32x32 accumulator layout
-//   each lane then holds 16 keys of a single query (lane % 32), so the row
-//   max and row sum are in-register reductions plus one exchange between
-//   lanes l and l+32.  The output is likewise accumulated transposed,
-//   O^T = V^T P^T: A = V^T (32 dims x 16 keys, from LDS), B = P^T taken
-//   straight from the score registers after exp and conversion to bf16.
-//   V is stored transposed in LDS, with keys permuted inside each group of 16
-//   so that every lane's 8 B-operand keys are one contiguous 16-byte read.
+//   A = K (32 keys x 16 dims, one 16-byte LDS read per lane), B = Q^T (16 dims
+//   x 32 queries, held in registers for the whole kernel).  In the 32x32
+//   accumulator layout each lane then holds 16 keys of a single query
+//   (lane % 32), so the row max and row sum are in-register reductions plus
+//   one exchange between lanes l and l^32.  The output is accumulated
+//   transposed too, O^T = V^T P^T: B = P^T comes straight from the score
+//   registers after exp2 and conversion to bf16; A = V^T is read from the
+//   row-major V tile with the LDS transpose read (ds_read_b64_tr_b16).
+//
+// LDS layout
+//   A K or V tile row (one key, D bf16) is D*2 bytes of 16-byte units; unit c
+//   of row `key` is stored at unit c ^ f(key).  The swizzles make the 16-byte
+//   K reads (16 consecutive keys, one unit) and the transpose reads of V
+//   (4 consecutive keys x 4 units) hit 16 distinct 16-byte bank groups.
+//
+// Pipeline
+//   Iteration i computes the scores of tile i+1 (MFMA) in the same basic block
+//   as the softmax of tile i (VALU), so the scheduler can interleave them, then
+//   accumulates P_i V_i.  The loads of K_{i+2} and V_{i+1} are in flight during
+//   the whole iteration.  The running maximum is raised only when a tile's
+//   maximum exceeds it by more than 2^8, so the output accumulator is rescaled
+//   on a handful of tiles only (probabilities stay below 2^8; the final
+//   normalisation divides the same factor out of OUT and the row sum).
 //
 // Accumulator layout of the 32x32 MFMA (lane l, register r):
 //   row i = 8*(r/4) + 4*(l/32) + (r%4), column j = l % 32.
@@ -38,8 +54,12 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+#define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
+#define GLOBAL_PTR(T, p) ((const __attribute__((address_space(1))) T*)(p))
 
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -49,13 +69,14 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Position of key k (0..15 inside a group of 16) in the transposed V tile:
-// 4-key blocks are stored in the order 0,2,1,3 so that lane group g of the
-// PV MFMA, which needs keys {4g..4g+3, 8+4g..8+4g+3}, reads 8 contiguous keys.
-__device__ __forceinline__ int vperm(int key) {
-  const int blk = (key >> 2) & 3;
-  const int pblk = ((blk & 1) << 1) | (blk >> 1);
-  return (key & ~15) | (pblk << 2) | (key & 3);
+// max / sum of x over lanes l and l^32 (the two lanes holding one query row)
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 template <int D, int QB, int NW, int BN>
@@ -66,22 +87,30 @@ struct Cfg {
   static constexpr int KB = BN / 32;          // 32-key blocks per key tile
   static constexpr int DB = D / 32;           // 32-dim blocks of the output
   static constexpr int PS = BN / 16;          // MFMA k-steps over a key tile
-  static constexpr int KST = D + 8;           // K tile row stride (elements)
-  static constexpr int VST = BN + 8;          // V^T tile row stride (elements)
-  static constexpr int KTILE = BN * KST;      // elements
-  static constexpr int VTILE = D * VST;
-  static constexpr int KCH = BN * D / 8;      // 16-byte chunks of a K tile
-  static constexpr int KCH_T = KCH / NT;      // per thread
-  static constexpr int VPAIRS = (BN / 2) * (D / 8);   // (key pair, 8 dims) items
-  static constexpr int VP_T = VPAIRS / NT;
-  static_assert(KCH % NT == 0 && VPAIRS % NT == 0, "tile not divisible by threads");
-  static_assert(BN % 32 == 0 && D % 32 == 0, "bad tile");
+  static constexpr int UNITS = D / 8;         // 16-byte units per tile row
+  static constexpr int ROWB = D * 2;          // bytes per tile row
+  static constexpr int TILEB = BN * ROWB;     // bytes per K or V tile
+  static constexpr int LOADS = TILEB / 1024;  // 1 KiB direct loads per tile
+  static constexpr int LOADS_W = LOADS / NW;  // per wave
+  static constexpr int ROWS_PER_LOAD = 1024 / ROWB;
+  static_assert(D == 64 || D == 128, "head dim");
+  static_assert(LOADS % NW == 0, "tile loads must split evenly over waves");
+  static_assert(BN % 32 == 0, "key tile");
 };
 
-template <int D, int QB, int NW, int BN>
-__global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(const AttnArgs a) {
+// unit swizzles (see the file comment): 16 consecutive keys reading the same
+// unit, and 4 consecutive keys x 4 consecutive units, are bank-group distinct
+template <int D> __device__ __forceinline__ int swz_k(int key) {
+  return D == 128 ? (key & 15) : ((key >> 1) & 7);
+}
+template <int D> __device__ __forceinline__ int swz_v(int key) {
+  return D == 128 ? ((key & 3) << 2) : (((key >> 1) & 1) << 2);
+}
+
+template <int D, int QB, int NW, int BN, int WPE>
+__global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs a) {
   using C = Cfg<D, QB, NW, BN>;
-  __shared__ __attribute__((aligned(16))) __bf16 smem[2 * (C::KTILE + C::VTILE)];
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[4 * C::TILEB];
 
   // ---- task decode: (selected partition, batch, head, query tile)
   const int task = xcd_remap(blockIdx.x, gridDim.x);
@@ -133,159 +162,171 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(const AttnArgs a) {
     for (int db = 0; db < C::DB; ++db) o[qb][db] = f32x16{};
   }
 
-  // ---- staging registers for one K/V tile
-  u32x4 kreg[C::KCH_T];
-  u32x4 vreg[C::VP_T][2];
-
-  auto load_tile = [&](int key0) {
+  // ---- direct global -> LDS tile loads.  Lane l of a 1 KiB load writes LDS
+  // unit l of that KiB, i.e. row l / UNITS, stored unit l % UNITS; it fetches
+  // the global unit that the swizzle maps there.  Rows past the end of the
+  // partition are clamped to its last key: their scores are masked to -inf and
+  // their probabilities are exactly 0, so any finite value will do, and every
+  // load stays inside the partition.
+  const int last_key = kv_len > 0 ? kv_len - 1 : 0;
+  const int ld_row = lane / C::UNITS;
+  const int ld_unit = lane % C::UNITS;
+  auto load_tile = [&](const __bf16* src, unsigned char* dst, int key0, bool is_k) {
 #pragma unroll
-    for (int i = 0; i < C::KCH_T; ++i) {
-      const int c = tid + i * C::NT;
-      const int key = c / (D / 8);
-      const int d0 = (c % (D / 8)) * 8;
-      if (key0 + key < kv_len)
-        kreg[i] = *(const u32x4*)(kg + (int64_t)(key0 + key) * HD + d0);
-      else
-        kreg[i] = u32x4{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int i = 0; i < C::VP_T; ++i) {
-      const int c = tid + i * C::NT;
-      const int kp = c % (BN / 2);
-      const int d0 = (c / (BN / 2)) * 8;
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int key = key0 + 2 * kp + e;
-        if (key < kv_len)
-          vreg[i][e] = *(const u32x4*)(vg + (int64_t)key * HD + d0);
-        else
-          vreg[i][e] = u32x4{0, 0, 0, 0};
-      }
+    for (int i = 0; i < C::LOADS_W; ++i) {
+      const int li = wave * C::LOADS_W + i;               // which KiB of the tile
+      const int row = li * C::ROWS_PER_LOAD + ld_row;     // tile row (key)
+      const int key = min(key0 + row, last_key);
+      const int unit = ld_unit ^ (is_k ? swz_k<D>(row) : swz_v<D>(row));
+      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(void, src + (int64_t)key * HD + unit * 8),
+                                       LDS_PTR(void, dst + li * 1024), 16, 0, 0);
     }
   };
 
-  auto store_tile = [&](int buf) {
-    __bf16* ks = smem + buf * (C::KTILE + C::VTILE);
-    __bf16* vs = ks + C::KTILE;
-#pragma unroll
-    for (int i = 0; i < C::KCH_T; ++i) {
-      const int c = tid + i * C::NT;
-      const int key = c / (D / 8);
-      const int d0 = (c % (D / 8)) * 8;
-      *(u32x4*)(ks + key * C::KST + d0) = kreg[i];
-    }
-#pragma unroll
-    for (int i = 0; i < C::VP_T; ++i) {
-      const int c = tid + i * C::NT;
-      const int kp = c % (BN / 2);
-      const int d0 = (c / (BN / 2)) * 8;
-      const int pos = vperm(2 * kp);   // keys 2kp, 2kp+1 stay adjacent
-      uint32_t* dst = (uint32_t*)(vs + d0 * C::VST + pos);
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const uint32_t x0 = vreg[i][0][w];   // dims d0+2w, d0+2w+1 of key 2kp
-        const uint32_t x1 = vreg[i][1][w];   // same dims of key 2kp+1
-        // dim d0+2w: (key 2kp, key 2kp+1) low halves; dim d0+2w+1: high halves
-        dst[(2 * w) * (C::VST / 2)] = (x0 & 0xffffu) | (x1 << 16);
-        dst[(2 * w + 1) * (C::VST / 2)] = (x0 >> 16) | (x1 & 0xffff0000u);
-      }
-    }
-  };
+  unsigned char* kbuf0 = smem;
+  unsigned char* kbuf1 = smem + C::TILEB;
+  unsigned char* vbuf0 = smem + 2 * C::TILEB;
+  unsigned char* vbuf1 = smem + 3 * C::TILEB;
 
-  const int n_tiles = (kv_len + BN - 1) / BN;
-  if (n_tiles > 0) {
-    load_tile(0);
-    store_tile(0);
+  // K A-operand: lane reads unit (2s + g) of row kb*32 + lr
+  const int krow_off = lr * C::ROWB;
+  const int kswz = swz_k<D>(lr);
+  // V^T A-operand by transpose reads: in each 16-lane group, source lane r
+  // points at row 4g + r/4 (+ 16s + 8hh) and dims 32db + 16*(group%2) + 4*(r%4);
+  // lane i of the group then receives 4 consecutive keys at dim 16*(group%2) + i.
+  const int grp = lane >> 4;
+  const int rr = lane & 15;
+  const int vrow = 4 * g + (rr >> 2);                       // + 16s + 8hh
+  const int vdim = 16 * (grp & 1) + 4 * (rr & 3);           // + 32db
+  int voff[C::DB];
+#pragma unroll
+  for (int db = 0; db < C::DB; ++db) {
+    const int dim = 32 * db + vdim;
+    const int unit = (dim >> 3) ^ swz_v<D>(vrow);           // swizzle depends on row % 4 only
+    voff[db] = vrow * C::ROWB + unit * 16 + (dim & 7) * 2;
   }
-  __syncthreads();
 
-  const float sl2 = a.scale_log2;
-
-  for (int it = 0; it < n_tiles; ++it) {
-    const int buf = it & 1;
-    const int key0 = it * BN;
-    if (it + 1 < n_tiles) load_tile(key0 + BN);
-
-    const __bf16* ks = smem + buf * (C::KTILE + C::VTILE);
-    const __bf16* vs = ks + C::KTILE;
-
-    // ---- S^T = K Q^T for the tile: sacc[kb][qb] covers keys kb*32..+32
-    f32x16 sacc[C::KB][QB];
+  // S^T = K Q^T of one key tile
+  auto qk = [&](const unsigned char* ks, f32x16 (&sacc)[C::KB][QB]) {
 #pragma unroll
     for (int kb = 0; kb < C::KB; ++kb) {
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) sacc[kb][qb] = f32x16{};
 #pragma unroll
       for (int s = 0; s < C::KS; ++s) {
-        const bf16x8 ka = *(const bf16x8*)(ks + (kb * 32 + lr) * C::KST + 16 * s + 8 * g);
+        const int unit = (2 * s + g) ^ kswz;                 // kb*32 keeps row % 16
+        const bf16x8 ka = *(const bf16x8*)(ks + kb * 32 * C::ROWB + krow_off + unit * 16);
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) sacc[kb][qb] = mfma32(ka, qf[qb][s], sacc[kb][qb]);
       }
     }
-
-    // ---- mask keys past the end of the partition (last tile only)
-    if (key0 + BN > kv_len) {
+  };
+  auto v_frag = [&](const unsigned char* vs, int s, int db) {
+    const unsigned char* p = vs + 16 * s * C::ROWB + voff[db];
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, p));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(LDS_PTR(s16x4, p + 8 * C::ROWB));
+    const u32x2 l2 = __builtin_bit_cast(u32x2, lo);
+    const u32x2 h2 = __builtin_bit_cast(u32x2, hi);
+    return __builtin_bit_cast(bf16x8, u32x4{l2[0], l2[1], h2[0], h2[1]});
+  };
+  // keys at or past the end of the partition -> -inf
+  auto mask_tail = [&](f32x16 (&sacc)[C::KB][QB], int key0) {
 #pragma unroll
-      for (int kb = 0; kb < C::KB; ++kb)
+    for (int kb = 0; kb < C::KB; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = key0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-          if (key >= kv_len) {
+      for (int r = 0; r < 16; ++r) {
+        const int key = key0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+        if (key >= kv_len) {
 #pragma unroll
-            for (int qb = 0; qb < QB; ++qb) sacc[kb][qb][r] = -INFINITY;
-          }
+          for (int qb = 0; qb < QB; ++qb) sacc[kb][qb][r] = -INFINITY;
         }
-    }
+      }
+  };
 
-    // ---- online softmax (base 2, scaled) and P^T fragments
-    bf16x8 pf[QB][C::PS];
+  const float sl2 = a.scale_log2;
+  constexpr float kLazy = 8.0f;
+  auto iteration = [&](int i, f32x16 (&scur)[C::KB][QB], f32x16 (&snxt)[C::KB][QB],
+                       const unsigned char* k_next, const unsigned char* v_cur,
+                       unsigned char* k_fill, unsigned char* v_fill) {
+    // K_{i+2} and V_{i+1} land in LDS while this iteration computes
+    load_tile(kg, k_fill, (i + 2) * BN, true);
+    load_tile(vg, v_fill, (i + 1) * BN, false);
+    qk(k_next, snxt);
+
+    float alpha[QB];
+    bool grow = false;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
       float mx = -INFINITY;
 #pragma unroll
       for (int kb = 0; kb < C::KB; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][qb][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mnew = fmaxf(m[qb], mx * sl2);
-      const float alpha = fast_exp2(m[qb] - mnew);
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, scur[kb][qb][r]);
+      mx = pair_max(mx) * sl2;
+      const float mnew = mx > m[qb] + kLazy ? mx : m[qb];
+      alpha[qb] = fast_exp2(m[qb] - mnew);
+      grow |= mnew != m[qb];
       m[qb] = mnew;
-      float ls = 0.f;
 #pragma unroll
       for (int kb = 0; kb < C::KB; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(__builtin_fmaf(sacc[kb][qb][r], sl2, -mnew));
-          sacc[kb][qb][r] = p;
-          ls += p;
-        }
-      l[qb] = l[qb] * alpha + ls;
+        for (int r = 0; r < 16; ++r) scur[kb][qb][r] = fast_exp2(__builtin_fmaf(scur[kb][qb][r], sl2, -mnew));
+    }
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
 #pragma unroll
-      for (int db = 0; db < C::DB; ++db) o[qb][db] *= alpha;
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) o[qb][db] *= alpha[qb];
+    }
+    bf16x8 pf[QB][C::PS];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      float ls = 0.f;
 #pragma unroll
       for (int kb = 0; kb < C::KB; ++kb)
 #pragma unroll
         for (int hh = 0; hh < 2; ++hh) {
           f32x8 x;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] = sacc[kb][qb][8 * hh + e];
+          for (int e = 0; e < 8; ++e) {
+            x[e] = scur[kb][qb][8 * hh + e];
+            ls += x[e];
+          }
           pf[qb][2 * kb + hh] = __builtin_convertvector(x, bf16x8);
         }
+      l[qb] = l[qb] * alpha[qb] + ls;
     }
-
-    // ---- O^T += V^T P^T
+    // O^T += V^T P^T
 #pragma unroll
     for (int s = 0; s < C::PS; ++s) {
 #pragma unroll
       for (int db = 0; db < C::DB; ++db) {
-        const bf16x8 va = *(const bf16x8*)(vs + (db * 32 + lr) * C::VST + 16 * s + 8 * g);
+        const bf16x8 va = v_frag(v_cur, s, db);
 #pragma unroll
         for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma32(va, pf[qb][s], o[qb][db]);
       }
     }
-
-    if (it + 1 < n_tiles) store_tile(buf ^ 1);
+    if ((i + 2) * BN > kv_len && (i + 1) * BN < kv_len) mask_tail(snxt, (i + 1) * BN);
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's tile loads have landed
     __syncthreads();
+  };
+
+  const int n_tiles = (kv_len + BN - 1) / BN;
+  f32x16 s0[C::KB][QB], s1[C::KB][QB];
+  if (n_tiles > 0) {
+    load_tile(kg, kbuf0, 0, true);
+    load_tile(vg, vbuf0, 0, false);
+    load_tile(kg, kbuf1, BN, true);
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();
+    qk(kbuf0, s0);
+    if (BN > kv_len) mask_tail(s0, 0);
+    __syncthreads();
+    // tile i: K_i in kbuf[i%2] (consumed one iteration early), V_i in vbuf[i%2]
+    for (int i = 0; i < n_tiles; i += 2) {
+      iteration(i, s0, s1, kbuf1, vbuf0, kbuf0, vbuf1);
+      if (i + 1 < n_tiles) iteration(i + 1, s1, s0, kbuf0, vbuf1, kbuf1, vbuf0);
+    }
   }
 
   // ---- epilogue: normalise, write OUT_j and LSE_j of slot j
@@ -293,7 +334,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(const AttnArgs a) {
   const int64_t slot_elems = (int64_t)a.B * a.q_len * HD;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    const float lt = l[qb] + __shfl_xor(l[qb], 32);
+    const float lt = pair_sum(l[qb]);
     const int64_t row = row0 + qb * 32 + lr;
     if (row < a.q_len) {
       const float inv = lt > 0.f ? 1.0f / lt : 0.f;
@@ -316,7 +357,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(const AttnArgs a) {
   }
 }
 
-template <int D, int QB, int NW, int BN>
+template <int D, int QB, int NW, int BN, int WPE>
 hipError_t launch_cfg(const AttnArgs& a0, hipStream_t s) {
   using C = Cfg<D, QB, NW, BN>;
   AttnArgs a = a0;
@@ -324,15 +365,25 @@ hipError_t launch_cfg(const AttnArgs& a0, hipStream_t s) {
   const int64_t nblk = (int64_t)a.q_tiles * a.H * a.B * a.n_sel;
   if (nblk <= 0) return hipSuccess;
   if (nblk > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN>), dim3((unsigned)nblk), dim3(C::NT), 0, s, a);
+  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, WPE>), dim3((unsigned)nblk), dim3(C::NT), 0, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
+// Tile configuration (query blocks per wave, waves per workgroup, keys per
+// tile, minimum waves per SIMD) per head dim; overridable at build time for
+// tuning sweeps.
+#ifndef DITANGO_D128_CFG
+#define DITANGO_D128_CFG 1, 8, 64, 2
+#endif
+#ifndef DITANGO_D64_CFG
+#define DITANGO_D64_CFG 1, 8, 64, 2
+#endif
+
 hipError_t launch_attn_bf16(const AttnArgs& a, int D, hipStream_t s) {
-  if (D == 128) return launch_cfg<128, 2, 4, 64>(a, s);
-  if (D == 64) return launch_cfg<64, 2, 4, 64>(a, s);
+  if (D == 128) return launch_cfg<128, DITANGO_D128_CFG>(a, s);
+  if (D == 64) return launch_cfg<64, DITANGO_D64_CFG>(a, s);
   return hipErrorInvalidValue;
 }
 
