@@ -35,16 +35,28 @@
 //
 // Pipeline
 //   Iteration i computes the scores of tile i+1 (MFMA) in the same basic block
-//   as the softmax of tile i (VALU), so the scheduler can interleave them, then
-//   accumulates P_i V_i.  The loads of K_{i+2} and V_{i+1} are in flight during
-//   the whole iteration.  The running maximum is raised only when a tile's
-//   maximum exceeds it by more than 2^8, so the output accumulator is rescaled
-//   on a handful of tiles only (probabilities stay below 2^8; the final
-//   normalisation divides the same factor out of OUT and the row sum).
+//   as the exponentials of tile i (VALU), then accumulates P_i V_i (MFMA)
+//   beside the row maximum of tile i+1 (VALU), so each block has both kinds of
+//   work for the scheduler to interleave.  The loads of K_{i+2} and V_{i+1}
+//   are in flight during the whole iteration.  The running maximum is raised
+//   only when a tile's maximum exceeds it by more than 2^8, so the output
+//   accumulator is rescaled on a handful of tiles only (probabilities stay
+//   below 2^8; the final normalisation divides the same factor out of OUT and
+//   the row sum).
 //
 // Accumulator layout of the 32x32 MFMA (lane l, register r):
 //   row i = 8*(r/4) + 4*(l/32) + (r%4), column j = l % 32.
 #include "internal.h"
+
+// Explicit instruction interleave hints in the main loop (build-time switch).
+#ifndef DITANGO_SCHED
+#define DITANGO_SCHED 0
+#endif
+// Software-pipelined main loop (scores of tile i+1 beside the softmax of
+// tile i) or the sequential one (build-time switch).
+#ifndef DITANGO_PIPE
+#define DITANGO_PIPE 1
+#endif
 
 namespace ditango {
 namespace {
@@ -69,6 +81,25 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// LDS byte address of a pointer into the workgroup's shared memory
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// 16-byte direct load global -> LDS for the wave: lane l's 16 bytes from `src`
+// land at LDS byte lds_base + 16*l.  Issued from inline assembly so that the
+// compiler does not order every later LDS read of this wave after it (it
+// cannot tell the DMA target apart from the tiles being read); completion is
+// awaited explicitly with s_waitcnt vmcnt before the workgroup barrier that
+// publishes the tile.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_base) {
+  const uint32_t base = __builtin_amdgcn_readfirstlane(lds_base);   // wave-uniform
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(base)
+               : "memory", "m0");
+}
+
 // max / sum of x over lanes l and l^32 (the two lanes holding one query row)
 __device__ __forceinline__ float pair_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -79,7 +110,7 @@ __device__ __forceinline__ float pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D, int QB, int NW, int BN>
+template <int D, int QB, int NW, int BN, int NBUF>
 struct Cfg {
   static constexpr int NT = NW * 64;          // threads per workgroup
   static constexpr int BM = NW * QB * 32;     // query rows per workgroup
@@ -93,6 +124,12 @@ struct Cfg {
   static constexpr int LOADS = TILEB / 1024;  // 1 KiB direct loads per tile
   static constexpr int LOADS_W = LOADS / NW;  // per wave
   static constexpr int ROWS_PER_LOAD = 1024 / ROWB;
+  static constexpr int PF = NBUF - 1;         // tiles loaded ahead of use
+  // vmcnt(n): tile loads a wave may leave in flight at the end of an
+  // iteration (those issued in the last PF-1 iterations)
+  static constexpr int VM_LEFT = (PF - 1) * 2 * LOADS_W;
+  static_assert(NBUF >= 2 && (NBUF & (NBUF - 1)) == 0, "ring size");
+  static_assert(VM_LEFT <= 63, "vmcnt range");
   static_assert(D == 64 || D == 128, "head dim");
   static_assert(LOADS % NW == 0, "tile loads must split evenly over waves");
   static_assert(BN % 32 == 0, "key tile");
@@ -107,10 +144,14 @@ template <int D> __device__ __forceinline__ int swz_v(int key) {
   return D == 128 ? ((key & 3) << 2) : (((key >> 1) & 1) << 2);
 }
 
-template <int D, int QB, int NW, int BN, int WPE>
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wave are outstanding (expcnt and lgkmcnt not waited for)
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
+
+template <int D, int QB, int NW, int BN, int NBUF, int WPE>
 __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs a) {
-  using C = Cfg<D, QB, NW, BN>;
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[4 * C::TILEB];
+  using C = Cfg<D, QB, NW, BN, NBUF>;
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];   // 2*NBUF tiles
 
   // ---- task decode: (selected partition, batch, head, query tile)
   const int task = xcd_remap(blockIdx.x, gridDim.x);
@@ -178,15 +219,13 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
       const int row = li * C::ROWS_PER_LOAD + ld_row;     // tile row (key)
       const int key = min(key0 + row, last_key);
       const int unit = ld_unit ^ (is_k ? swz_k<D>(row) : swz_v<D>(row));
-      __builtin_amdgcn_global_load_lds(GLOBAL_PTR(void, src + (int64_t)key * HD + unit * 8),
-                                       LDS_PTR(void, dst + li * 1024), 16, 0, 0);
+      lds_dma16(src + (int64_t)key * HD + unit * 8, lds_addr(dst + li * 1024));
     }
   };
 
-  unsigned char* kbuf0 = smem;
-  unsigned char* kbuf1 = smem + C::TILEB;
-  unsigned char* vbuf0 = smem + 2 * C::TILEB;
-  unsigned char* vbuf1 = smem + 3 * C::TILEB;
+  // rings of NBUF K tiles and NBUF V tiles: tile t lives in slot t % NBUF
+  auto kbuf = [&](int t) { return smem + (t & (NBUF - 1)) * C::TILEB; };
+  auto vbuf = [&](int t) { return smem + (NBUF + (t & (NBUF - 1))) * C::TILEB; };
 
   // K A-operand: lane reads unit (2s + g) of row kb*32 + lr
   const int krow_off = lr * C::ROWB;
@@ -245,15 +284,11 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
 
   const float sl2 = a.scale_log2;
   constexpr float kLazy = 8.0f;
-  auto iteration = [&](int i, f32x16 (&scur)[C::KB][QB], f32x16 (&snxt)[C::KB][QB],
-                       const unsigned char* k_next, const unsigned char* v_cur,
-                       unsigned char* k_fill, unsigned char* v_fill) {
-    // K_{i+2} and V_{i+1} land in LDS while this iteration computes
-    load_tile(kg, k_fill, (i + 2) * BN, true);
-    load_tile(vg, v_fill, (i + 1) * BN, false);
-    qk(k_next, snxt);
-
-    float alpha[QB];
+  // Row maximum of a score tile (scaled, base 2) and the lazy update of the
+  // running maximum m: m moves only when the tile maximum exceeds it by more
+  // than kLazy.  Returns whether any lane of the wave moved its m; alpha gets
+  // the factor exp2(m_old - m_new) that rescales O and l.
+  auto update_max = [&](f32x16 (&sc)[C::KB][QB], float (&alpha)[QB], bool valid) {
     bool grow = false;
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -261,23 +296,36 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
 #pragma unroll
       for (int kb = 0; kb < C::KB; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, scur[kb][qb][r]);
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][qb][r]);
       mx = pair_max(mx) * sl2;
-      const float mnew = mx > m[qb] + kLazy ? mx : m[qb];
+      const float mnew = (valid && mx > m[qb] + kLazy) ? mx : m[qb];
       alpha[qb] = fast_exp2(m[qb] - mnew);
       grow |= mnew != m[qb];
       m[qb] = mnew;
-#pragma unroll
-      for (int kb = 0; kb < C::KB; ++kb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) scur[kb][qb][r] = fast_exp2(__builtin_fmaf(scur[kb][qb][r], sl2, -mnew));
+      l[qb] *= alpha[qb];
     }
-    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-        for (int db = 0; db < C::DB; ++db) o[qb][db] *= alpha[qb];
-    }
+    return __builtin_amdgcn_ballot_w64(grow) != 0;
+  };
+
+  // One pipelined iteration over key tile i.  On entry S_i holds the scores
+  // of tile i, the running maximum already covers them, and O, l are scaled
+  // to it.  Block A: the MFMAs of S_{i+1} = K_{i+1} Q^T run while the VALU
+  // turns S_i into probabilities P_i (exp2, row sums, bf16).  Block B: the
+  // MFMAs of O += V_i P_i run while the VALU takes the row maximum of S_{i+1}.
+  auto iteration = [&](int i, f32x16 (&scur)[C::KB][QB], f32x16 (&snxt)[C::KB][QB]) {
+    const unsigned char* k_next = kbuf(i + 1);
+    const unsigned char* v_cur = vbuf(i);
+    // Tile i is the partition's last and partial: mask its keys past the end.
+    // The masking waits until here so that the maximum taken in the previous
+    // iteration could sit beside the PV MFMAs; it is unaffected, because the
+    // rows past the end repeat the last key, which is in this tile.
+    if ((i + 1) * BN > kv_len) mask_tail(scur, i * BN);
+    // K_{i+1+PF} and V_{i+PF} land in LDS during the next PF iterations; they
+    // overwrite K_{i+1+PF-NBUF} and V_{i+PF-NBUF}, consumed before the last
+    // barrier
+    load_tile(kg, kbuf(i + 1 + C::PF), (i + 1 + C::PF) * BN, true);
+    load_tile(vg, vbuf(i + C::PF), (i + C::PF) * BN, false);
+    qk(k_next, snxt);
     bf16x8 pf[QB][C::PS];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -289,13 +337,14 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
           f32x8 x;
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            x[e] = scur[kb][qb][8 * hh + e];
+            x[e] = fast_exp2(__builtin_fmaf(scur[kb][qb][8 * hh + e], sl2, -m[qb]));
             ls += x[e];
           }
           pf[qb][2 * kb + hh] = __builtin_convertvector(x, bf16x8);
         }
-      l[qb] = l[qb] * alpha[qb] + ls;
+      l[qb] += ls;
     }
+    const bool has_next = (i + 1) * BN < kv_len;
     // O^T += V^T P^T
 #pragma unroll
     for (int s = 0; s < C::PS; ++s) {
@@ -306,28 +355,120 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
         for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma32(va, pf[qb][s], o[qb][db]);
       }
     }
-    if ((i + 2) * BN > kv_len && (i + 1) * BN < kv_len) mask_tail(snxt, (i + 1) * BN);
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's tile loads have landed
+#if DITANGO_SCHED
+    // Interleave (one scheduling region): the QK^T MFMAs of tile i+1, each
+    // beside one K-operand LDS read, two FMAs and two exp2 of tile i; then
+    // the PV MFMAs, each beside two transpose reads and the VALU work of the
+    // row sums, bf16 conversion and the row maximum of tile i+1.
+#pragma unroll
+    for (int k = 0; k < C::KB * C::KS * QB; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   // VALU
+      __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);   // transcendental
+    }
+#pragma unroll
+    for (int k = 0; k < C::PS * C::DB * QB; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // VALU
+    }
+#endif
+    float alpha[QB];
+    if (update_max(snxt, alpha, has_next)) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) o[qb][db] *= alpha[qb];
+    }
+    // K_{i+2} and V_{i+1}, used by the next iteration, have landed for this
+    // wave; the barrier makes that true for the whole workgroup
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));
     __syncthreads();
   };
 
   const int n_tiles = (kv_len + BN - 1) / BN;
+#if DITANGO_PIPE
   f32x16 s0[C::KB][QB], s1[C::KB][QB];
   if (n_tiles > 0) {
-    load_tile(kg, kbuf0, 0, true);
-    load_tile(vg, vbuf0, 0, false);
-    load_tile(kg, kbuf1, BN, true);
-    __builtin_amdgcn_s_waitcnt(0x0F70);
+    // K_0, then the loads iterations -PF..-1 would have issued, in the same
+    // order as the loop issues them
+    load_tile(kg, kbuf(0), 0, true);
+#pragma unroll
+    for (int j = -C::PF; j < 0; ++j) {
+      load_tile(kg, kbuf(j + 1 + C::PF), (j + 1 + C::PF) * BN, true);
+      load_tile(vg, vbuf(j + C::PF), (j + C::PF) * BN, false);
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_0, K_1, V_0 have landed
     __syncthreads();
-    qk(kbuf0, s0);
-    if (BN > kv_len) mask_tail(s0, 0);
+    qk(kbuf(0), s0);
+    float alpha0[QB];
+    update_max(s0, alpha0, true);          // O and l are still zero
     __syncthreads();
-    // tile i: K_i in kbuf[i%2] (consumed one iteration early), V_i in vbuf[i%2]
+    // K_i is consumed one iteration early (scores of the next tile)
     for (int i = 0; i < n_tiles; i += 2) {
-      iteration(i, s0, s1, kbuf1, vbuf0, kbuf0, vbuf1);
-      if (i + 1 < n_tiles) iteration(i + 1, s1, s0, kbuf0, vbuf1, kbuf1, vbuf0);
+      iteration(i, s0, s1);
+      if (i + 1 < n_tiles) iteration(i + 1, s1, s0);
     }
   }
+#else
+  // Sequential form: each iteration takes the scores, softmax and PV of one
+  // tile; the two waves sharing a SIMD overlap each other's phases.
+  if (n_tiles > 0) {
+#pragma unroll
+    for (int j = -C::PF; j < 0; ++j) {
+      load_tile(kg, kbuf(j + C::PF), (j + C::PF) * BN, true);
+      load_tile(vg, vbuf(j + C::PF), (j + C::PF) * BN, false);
+    }
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_0, V_0 have landed
+    __syncthreads();
+    for (int i = 0; i < n_tiles; ++i) {
+      load_tile(kg, kbuf(i + C::PF), (i + C::PF) * BN, true);
+      load_tile(vg, vbuf(i + C::PF), (i + C::PF) * BN, false);
+      f32x16 sc[C::KB][QB];
+      qk(kbuf(i), sc);
+      if ((i + 1) * BN > kv_len) mask_tail(sc, i * BN);
+      float alpha[QB];
+      if (update_max(sc, alpha, true)) {
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+          for (int db = 0; db < C::DB; ++db) o[qb][db] *= alpha[qb];
+      }
+      bf16x8 pf[QB][C::PS];
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        float ls = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < C::KB; ++kb)
+#pragma unroll
+          for (int hh = 0; hh < 2; ++hh) {
+            f32x8 x;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              x[e] = fast_exp2(__builtin_fmaf(sc[kb][qb][8 * hh + e], sl2, -m[qb]));
+              ls += x[e];
+            }
+            pf[qb][2 * kb + hh] = __builtin_convertvector(x, bf16x8);
+          }
+        l[qb] += ls;
+      }
+      const unsigned char* v_cur = vbuf(i);
+#pragma unroll
+      for (int s = 0; s < C::PS; ++s) {
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) {
+          const bf16x8 va = v_frag(v_cur, s, db);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma32(va, pf[qb][s], o[qb][db]);
+        }
+      }
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_{i+1}, V_{i+1} have landed
+      __syncthreads();
+    }
+  }
+#endif
+
 
   // ---- epilogue: normalise, write OUT_j and LSE_j of slot j
   __bf16* outg = (__bf16*)a.out_states;
@@ -357,28 +498,33 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   }
 }
 
-template <int D, int QB, int NW, int BN, int WPE>
+template <int D, int QB, int NW, int BN, int NBUF, int WPE>
 hipError_t launch_cfg(const AttnArgs& a0, hipStream_t s) {
-  using C = Cfg<D, QB, NW, BN>;
+  using C = Cfg<D, QB, NW, BN, NBUF>;
+  const size_t lds = (size_t)2 * NBUF * C::TILEB;
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE>,
+      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (attr != hipSuccess) return attr;
   AttnArgs a = a0;
   a.q_tiles = (int)((a.q_len + C::BM - 1) / C::BM);
   const int64_t nblk = (int64_t)a.q_tiles * a.H * a.B * a.n_sel;
   if (nblk <= 0) return hipSuccess;
   if (nblk > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, WPE>), dim3((unsigned)nblk), dim3(C::NT), 0, s, a);
+  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE>), dim3((unsigned)nblk), dim3(C::NT), lds, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 // Tile configuration (query blocks per wave, waves per workgroup, keys per
-// tile, minimum waves per SIMD) per head dim; overridable at build time for
-// tuning sweeps.
+// tile, K/V ring size, minimum waves per SIMD) per head dim; overridable at
+// build time for tuning sweeps.
 #ifndef DITANGO_D128_CFG
-#define DITANGO_D128_CFG 1, 8, 64, 2
+#define DITANGO_D128_CFG 1, 8, 64, 2, 2
 #endif
 #ifndef DITANGO_D64_CFG
-#define DITANGO_D64_CFG 1, 8, 64, 2
+#define DITANGO_D64_CFG 1, 8, 64, 2, 2
 #endif
 
 hipError_t launch_attn_bf16(const AttnArgs& a, int D, hipStream_t s) {
