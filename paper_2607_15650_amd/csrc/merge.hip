@@ -4,9 +4,8 @@
 //   M = max_j LSE_j, LSE = M + log sum_j e^{LSE_j - M}, OUT = sum_j e^{LSE_j - LSE} OUT_j,
 // over a list of cached/fresh state slots.  Pure streaming: every OUT slot is
 // read once and the output written once, so the kernel is bound by HBM
-// bandwidth.  Each thread owns 16 bytes of one output row per iteration and
-// issues the loads of all listed slots before using them, so that enough
-// bytes are in flight to cover HBM latency.
+// bandwidth.  The state loads are issued first; the weights of a row are
+// reduced across the lanes that own the row while they are in flight.
 //
 // contrib: per-row weights W_j = e^{LSE_j - LSE} (w_i of Sec. 4.1.1; the
 // anchor weights of Eq. lse_weight) and their mean over all rows per
@@ -33,7 +32,7 @@ template <> struct Vec8<__bf16> {
     return __builtin_convertvector(x, f32x8);
   }
   static __device__ __forceinline__ void store(__bf16* p, const f32x8& v) {
-    *(bf16x8*)p = __builtin_convertvector(v, bf16x8);
+    __builtin_nontemporal_store(__builtin_convertvector(v, bf16x8), (bf16x8*)p);
   }
 };
 template <> struct Vec8<float> {
@@ -43,74 +42,93 @@ template <> struct Vec8<float> {
     return f32x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
   }
   static __device__ __forceinline__ void store(float* p, const f32x8& v) {
-    *(f32x4*)p = f32x4{v[0], v[1], v[2], v[3]};
-    *(f32x4*)(p + 4) = f32x4{v[4], v[5], v[6], v[7]};
+    __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, (f32x4*)p);
+    __builtin_nontemporal_store(f32x4{v[4], v[5], v[6], v[7]}, (f32x4*)(p + 4));
   }
 };
 
 constexpr int kMergeThreads = 256;
-constexpr int kMergeUnroll = 8;   // slots loaded per batch
+constexpr int kMergeBatch = 8;    // slots whose loads are in flight together
 
+// Each thread owns one 8-element chunk of one row (row = (b*q_len + r)*H + h,
+// rows contiguous in every slot), so the CPR = D/8 lanes of a row are
+// consecutive lanes of one wave.  The thread first issues the state loads of
+// the first batch of slots; lane k of the row loads LSE_j for j = k, k+CPR, ...
+// at the same time.  The row's maximum, log-sum-exp and weights are then
+// reduced across its CPR lanes with shuffles (no LDS, no barrier), and every
+// lane forms OUT = sum_j w_j OUT_j in float32.
 template <typename TS, typename TO, int D>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a) {
-  constexpr int CPR = D / 8;                      // 8-element chunks per row
-  const int64_t n_chunks = a.rows * CPR;
+  constexpr int CPR = D / 8;                      // chunks (lanes) per row
+  constexpr int LPL = (kMaxParts + CPR - 1) / CPR;   // LSEs per lane, upper bound
+  const int64_t c = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x;
+  const bool live = c < a.rows * CPR;
+  const int64_t row = live ? c / CPR : 0;
+  const int ch = (int)(c % CPR);
   const int64_t slot_elems = a.rows * D;
   const int64_t lse_slot = (int64_t)a.B * a.H * a.q_len;
-  const TS* __restrict__ st = (const TS*)a.states;
-  TO* __restrict__ out = (TO*)a.out;
+  const TS* __restrict__ st = (const TS*)a.states + row * D + ch * 8;
 
-  for (int64_t c = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x; c < n_chunks;
-       c += (int64_t)gridDim.x * kMergeThreads) {
-    const int64_t row = c / CPR;                  // row = (b*q_len + r)*H + h
-    const int64_t e0 = c * 8;
-    const int h = (int)(row % a.H);
-    const int64_t br = row / a.H;
-    const int64_t r = br % a.q_len;
-    const int64_t b = br / a.q_len;
-    const int64_t li = (b * a.H + h) * a.q_len + r;
+  f32x8 x[kMergeBatch];
+#pragma unroll
+  for (int u = 0; u < kMergeBatch; ++u)
+    x[u] = (live && u < a.n) ? Vec8<TS>::load(st + (int64_t)a.slots[u] * slot_elems) : f32x8{};
 
-    float mx = -INFINITY;
-    for (int j = 0; j < a.n; ++j) mx = fmaxf(mx, a.lse[(int64_t)a.slots[j] * lse_slot + li]);
-    f32x8 acc = f32x8{};
-    float lse = -INFINITY;
-    if (mx != -INFINITY) {
-      float tot = 0.f;
-      for (int j = 0; j < a.n; ++j)
-        tot += __builtin_amdgcn_exp2f((a.lse[(int64_t)a.slots[j] * lse_slot + li] - mx) * kLog2e);
-      const float inv = 1.0f / tot;
-      lse = mx + __builtin_amdgcn_logf(tot) * kLn2;
-      for (int j0 = 0; j0 < a.n; j0 += kMergeUnroll) {
-        f32x8 x[kMergeUnroll];
-        float w[kMergeUnroll];
+  const int h = (int)(row % a.H);
+  const int64_t br = row / a.H;
+  const int64_t li = ((br / a.q_len) * a.H + h) * a.q_len + br % a.q_len;
+  float lv[LPL];
+  float mx = -INFINITY;
 #pragma unroll
-        for (int u = 0; u < kMergeUnroll; ++u) {
-          const int j = j0 + u;
-          if (j < a.n) {
-            const int64_t s = a.slots[j];
-            x[u] = Vec8<TS>::load(st + s * slot_elems + e0);
-            w[u] = __builtin_amdgcn_exp2f((a.lse[s * lse_slot + li] - mx) * kLog2e) * inv;
-          } else {
-            x[u] = f32x8{};
-            w[u] = 0.f;
-          }
-        }
+  for (int k = 0; k < LPL; ++k) {
+    const int j = ch + k * CPR;
+    lv[k] = (live && j < a.n) ? a.lse[(int64_t)a.slots[j] * lse_slot + li] : -INFINITY;
+    mx = fmaxf(mx, lv[k]);
+  }
 #pragma unroll
-        for (int u = 0; u < kMergeUnroll; ++u) acc += w[u] * x[u];
-      }
-    }
-    Vec8<TO>::store(out + e0, acc);
-    if (a.lse_out != nullptr && (c % CPR) == 0) a.lse_out[li] = lse;
+  for (int off = CPR / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, CPR));
+  float tot = 0.f;
+#pragma unroll
+  for (int k = 0; k < LPL; ++k) {
+    lv[k] = mx == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((lv[k] - mx) * kLog2e);
+    tot += lv[k];
+  }
+#pragma unroll
+  for (int off = CPR / 2; off > 0; off >>= 1) tot += __shfl_xor(tot, off, CPR);
+  const float inv = tot > 0.f ? 1.0f / tot : 0.f;
+  const float lse = tot > 0.f ? mx + __builtin_amdgcn_logf(tot) * kLn2 : -INFINITY;
+
+  // weight of slot j sits in lane j % CPR of the row, entry j / CPR
+  auto weight = [&](int j) {
+    float v = lv[0];
+#pragma unroll
+    for (int k = 1; k < LPL; ++k)
+      if (j / CPR == k) v = lv[k];
+    return __shfl(v, j % CPR, CPR) * inv;
+  };
+  f32x8 acc = f32x8{};
+#pragma unroll
+  for (int u = 0; u < kMergeBatch; ++u)
+    if (u < a.n) acc += weight(u) * x[u];
+  for (int j0 = kMergeBatch; j0 < a.n; j0 += kMergeBatch) {
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u)
+      x[u] = (live && j0 + u < a.n) ? Vec8<TS>::load(st + (int64_t)a.slots[j0 + u] * slot_elems) : f32x8{};
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u)
+      if (j0 + u < a.n) acc += weight(j0 + u) * x[u];
+  }
+  if (live) {
+    Vec8<TO>::store((TO*)a.out + row * D + ch * 8, acc);
+    if (a.lse_out != nullptr && ch == 0) a.lse_out[li] = lse;
   }
 }
 
 template <typename TS, typename TO, int D>
 hipError_t launch_merge_t(const MergeArgs& a, hipStream_t s) {
-  const int64_t n_chunks = a.rows * (D / 8);
-  if (n_chunks == 0) return hipSuccess;
-  int64_t blocks = (n_chunks + kMergeThreads - 1) / kMergeThreads;
-  const int64_t cap = 256 * 64;   // grid-stride beyond 64 workgroups per CU
-  if (blocks > cap) blocks = cap;
+  const int64_t blocks = (a.rows * (D / 8) + kMergeThreads - 1) / kMergeThreads;
+  if (blocks == 0) return hipSuccess;
+  if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   hipLaunchKernelGGL((merge_kernel<TS, TO, D>), dim3((unsigned)blocks), dim3(kMergeThreads), 0, s, a);
   return hipGetLastError();
 }
