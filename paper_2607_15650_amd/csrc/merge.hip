@@ -57,10 +57,14 @@ constexpr int kMergeBatch = 8;    // slots whose loads are in flight together
 // at the same time.  The row's maximum, log-sum-exp and weights are then
 // reduced across its CPR lanes with shuffles (no LDS, no barrier), and every
 // lane forms OUT = sum_j w_j OUT_j in float32.
-template <typename TS, typename TO, int D>
+// NS > 0: the slot count is the compile-time constant NS (the common
+// partition counts get their own instantiation, free of run-time loop bounds);
+// NS == 0: any count up to kMaxParts, read from the arguments.
+template <typename TS, typename TO, int D, int NS>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a) {
   constexpr int CPR = D / 8;                      // chunks (lanes) per row
-  constexpr int LPL = (kMaxParts + CPR - 1) / CPR;   // LSEs per lane, upper bound
+  constexpr int LPL = ((NS > 0 ? NS : kMaxParts) + CPR - 1) / CPR;   // LSEs per lane
+  const int n = NS > 0 ? NS : a.n;
   const int64_t c = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x;
   const bool live = c < a.rows * CPR;
   const int64_t row = live ? c / CPR : 0;
@@ -72,7 +76,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   f32x8 x[kMergeBatch];
 #pragma unroll
   for (int u = 0; u < kMergeBatch; ++u)
-    x[u] = (live && u < a.n) ? Vec8<TS>::load(st + (int64_t)a.slots[u] * slot_elems) : f32x8{};
+    x[u] = (live && u < n) ? Vec8<TS>::load(st + (int64_t)a.slots[u] * slot_elems) : f32x8{};
 
   const int h = (int)(row % a.H);
   const int64_t br = row / a.H;
@@ -82,7 +86,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
 #pragma unroll
   for (int k = 0; k < LPL; ++k) {
     const int j = ch + k * CPR;
-    lv[k] = (live && j < a.n) ? a.lse[(int64_t)a.slots[j] * lse_slot + li] : -INFINITY;
+    lv[k] = (live && j < n) ? a.lse[(int64_t)a.slots[j] * lse_slot + li] : -INFINITY;
     mx = fmaxf(mx, lv[k]);
   }
 #pragma unroll
@@ -109,14 +113,14 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   f32x8 acc = f32x8{};
 #pragma unroll
   for (int u = 0; u < kMergeBatch; ++u)
-    if (u < a.n) acc += weight(u) * x[u];
-  for (int j0 = kMergeBatch; j0 < a.n; j0 += kMergeBatch) {
+    if (u < n) acc += weight(u) * x[u];
+  for (int j0 = kMergeBatch; j0 < n; j0 += kMergeBatch) {
 #pragma unroll
     for (int u = 0; u < kMergeBatch; ++u)
-      x[u] = (live && j0 + u < a.n) ? Vec8<TS>::load(st + (int64_t)a.slots[j0 + u] * slot_elems) : f32x8{};
+      x[u] = (live && j0 + u < n) ? Vec8<TS>::load(st + (int64_t)a.slots[j0 + u] * slot_elems) : f32x8{};
 #pragma unroll
     for (int u = 0; u < kMergeBatch; ++u)
-      if (j0 + u < a.n) acc += weight(j0 + u) * x[u];
+      if (j0 + u < n) acc += weight(j0 + u) * x[u];
   }
   if (live) {
     Vec8<TO>::store((TO*)a.out + row * D + ch * 8, acc);
@@ -129,7 +133,13 @@ hipError_t launch_merge_t(const MergeArgs& a, hipStream_t s) {
   const int64_t blocks = (a.rows * (D / 8) + kMergeThreads - 1) / kMergeThreads;
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((merge_kernel<TS, TO, D>), dim3((unsigned)blocks), dim3(kMergeThreads), 0, s, a);
+  const dim3 g((unsigned)blocks), t(kMergeThreads);
+  switch (a.n) {
+    case 4: hipLaunchKernelGGL((merge_kernel<TS, TO, D, 4>), g, t, 0, s, a); break;
+    case 8: hipLaunchKernelGGL((merge_kernel<TS, TO, D, 8>), g, t, 0, s, a); break;
+    case 16: hipLaunchKernelGGL((merge_kernel<TS, TO, D, 16>), g, t, 0, s, a); break;
+    default: hipLaunchKernelGGL((merge_kernel<TS, TO, D, 0>), g, t, 0, s, a); break;
+  }
   return hipGetLastError();
 }
 
