@@ -33,6 +33,13 @@ PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3        # MI355X fp32 MFMA / vector
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 
+# HBM bytes per launch of the attention kernel at the default workload, from
+# rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE (each scaled so that a plain 1 GiB
+# elementwise copy reads / writes 1 GiB), keyed by the SHA-256 prefix of the
+# kernel source they were taken on; reported only while the source matches.
+ATTN_TRAFFIC = {"src_sha256_16": "6416ca39a158485f", "workload": "videodit_bf16_h40_d128_s75600_p8",
+                "fetch_bytes": 759960 * 1024 * 2.0, "write_bytes": 314640 * 1024 * 1.0}
+
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
@@ -43,6 +50,10 @@ def parse():
     ap.add_argument("--select", default=None, help="comma-separated fresh partitions (default: the workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
+    ap.add_argument("--threshold", type=float, default=None,
+                    help="planner-driven workload: anchor-weight threshold (default: the workload's)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time the step for each selection of the workload's sweep (long-context workload)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before timing, run one plain elementwise copy of this many MiB "
                          "(the reference kernel that scales profiler byte counters)")
@@ -59,6 +70,21 @@ def algorithmic(w, select):
     merge_bytes = w.P * rows * (w.D * s_state + 4) + rows * (w.D * s_state + 4)
     contrib_bytes = (w.P + 1) * rows * 4 + w.P * 4
     return flops, merge_bytes, contrib_bytes
+
+
+def attn_traffic(w, select):
+    """Profiled HBM bytes per attention launch, or None when the kernel source,
+    the workload or the selection differs from the one the counters were
+    taken on."""
+    import hashlib
+    src = os.path.join(ROOT, "paper_2607_15650_amd", "csrc", "attn_bf16.hip")
+    try:
+        h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except OSError:
+        return None
+    if h != ATTN_TRAFFIC["src_sha256_16"] or w.name != ATTN_TRAFFIC["workload"] or tuple(select) != w.select:
+        return None
+    return ATTN_TRAFFIC["fetch_bytes"] + ATTN_TRAFFIC["write_bytes"]
 
 
 def cpu_baseline(w, x, select, target_s):
@@ -110,6 +136,133 @@ def cpu_baseline(w, x, select, target_s):
     return n, t, per_step_s, cores
 
 
+def multistep(args, w):
+    """Planner-driven run: every query block, w.steps denoising steps, anchors
+    compute every partition, other steps the query partition plus every
+    partition whose anchor weight exceeds w.threshold.  Reports the selective
+    attention time, the all-fresh time and the drift of the selective output
+    from fresh full attention at every step."""
+    import numpy as np
+    import torch
+    from fixtures import bf16_bits, gen_qkv, gen_evolved
+    from paper_2607_15650_amd import api
+    from paper_2607_15650_amd.planner import AnchorPlanner
+    from paper_2607_15650_amd.step import SelectiveAttention
+
+    offs = w.offsets
+    blocks = list(range(w.P))
+    g = lambda a: torch.from_numpy(bf16_bits(a).view(np.int16)).view(torch.bfloat16).cuda()
+    sa = SelectiveAttention(w.B, w.H, w.D, offs, w.scale, torch.bfloat16)
+    ref = SelectiveAttention(w.B, w.H, w.D, offs, w.scale, torch.bfloat16)
+    planners = {qb: AnchorPlanner(w.P, qb, w.anchors, w.threshold) for qb in blocks}
+    x = gen_qkv(w, with_prev=False)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    t_sel = t_full = 0.0
+    flops_sel = flops_full = 0.0
+    per_step = []
+    for s in range(w.steps):
+        q, k, v = g(x["q"]), g(x["k"]), g(x["v"])
+        torch.cuda.synchronize()
+        masks, drift, maxabs = [], [], []
+        for qb in blocks:
+            mask = planners[qb].select(s)
+            L = offs[qb + 1] - offs[qb]
+            e0, e1, e2 = ev(), ev(), ev()
+            e0.record()
+            out, lse, wp = sa.step(s, qb, q, k, v, mask)
+            e1.record()
+            fo, fl, _ = ref.step(s, qb, q, k, v, [1] * w.P)
+            e2.record()
+            torch.cuda.synchronize()
+            t_sel += e0.elapsed_time(e1)
+            t_full += e1.elapsed_time(e2)
+            keys = sum(offs[j + 1] - offs[j] for j in range(w.P) if mask[j])
+            flops_sel += 4.0 * w.B * w.H * L * w.D * keys
+            flops_full += 4.0 * w.B * w.H * L * w.D * offs[-1]
+            planners[qb].observe(s, wp.cpu().numpy())
+            d = (out.float() - fo.float())
+            drift.append(float(d.norm() / fo.float().norm()))
+            maxabs.append(float(d.abs().max()))
+            masks.append("".join(str(m) for m in mask))
+        per_step.append({"step": s, "anchor": s in w.anchors, "masks": masks,
+                         "drift_rel_l2_max": max(drift), "drift_maxabs_max": max(maxabs)})
+        print(f"[bench] step {s} masks {masks} drift {max(drift):.3e}", file=sys.stderr, flush=True)
+        if s + 1 < w.steps:
+            x = gen_evolved(w, x, s)
+    res = {
+        "metric": METRIC, "value": flops_sel / (t_sel * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": w.steps, "warmup": 0, "ms_per_step": t_sel / w.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic (seeded; each step adds 0.03*N(0,1) to Q, K, V)",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "D": w.D, "S": w.S, "P": w.P,
+                   "query_blocks": len(blocks), "anchors": list(w.anchors), "threshold": w.threshold},
+        "selective_ms_total": t_sel, "all_fresh_ms_total": t_full, "speedup_vs_all_fresh": t_full / t_sel,
+        "computed_fraction": flops_sel / flops_full, "per_step": per_step,
+        "note": "times include every call's launch on the stream; each block's step is synchronised "
+                "to read its weights back for the planner",
+    }
+    print(json.dumps(res), flush=True)
+
+
+def sweep(args, w):
+    """Step time for each selection of the workload's sweep (nearest-first sizes)."""
+    import numpy as np
+    import torch
+    from fixtures import bf16_bits, gen_qkv
+    from paper_2607_15650_amd import api
+
+    offs = w.offsets
+    qa, qb = offs[w.q], offs[w.q + 1]
+    x = gen_qkv(w, with_prev=True)
+    g = lambda a: torch.from_numpy(bf16_bits(np.ascontiguousarray(a)).view(np.int16)).view(torch.bfloat16).cuda()
+    q, k, v = g(x["q"][:, qa:qb]), g(x["k"]), g(x["v"])
+    qp, kp, vp = g(x["q_prev"][:, qa:qb]), g(x["k_prev"]), g(x["v_prev"])
+    del x
+    L = w.q_len
+    st = torch.empty((w.P, w.B, L, w.H, w.D), dtype=torch.bfloat16, device="cuda")
+    ls = torch.empty((w.P, w.B, w.H, L), dtype=torch.float32, device="cuda")
+    out = torch.empty((w.B, L, w.H, w.D), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((w.B, w.H, L), dtype=torch.float32, device="cuda")
+    wp = torch.empty(w.P, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(16, api.contrib_workspace_bytes(w.B, w.H, L, w.P)), dtype=torch.uint8, device="cuda")
+    api.attn_partition_states(qp, kp, vp, offs, [1] * w.P, w.scale, st, ls)
+    rows = []
+    for sel in w.sweep:
+        mask = [1 if j in sel else 0 for j in range(w.P)]
+
+        def step():
+            api.attn_partition_states(q, k, v, offs, mask, w.scale, st, ls)
+            api.merge_states(st, ls, out, lse)
+            api.contrib(ls, lse, wp, ws)
+        for _ in range(args.warmup):
+            step()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        flops = algorithmic(w, sel)[0]
+        rows.append({"k": len(sel), "fraction": len(sel) / w.P, "ms_per_step": ms,
+                     "tflops": flops / (ms * 1e-3) / 1e12})
+        print(f"[bench] k={len(sel)} {ms:.3f} ms", file=sys.stderr, flush=True)
+    ks = np.array([r["fraction"] for r in rows])
+    ts = np.array([r["ms_per_step"] for r in rows])
+    slope, icpt = np.polyfit(ks, ts, 1)
+    full = rows[-1]
+    res = {
+        "metric": METRIC, "value": full["tflops"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": full["ms_per_step"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "D": w.D, "S": w.S, "P": w.P,
+                   "query_partition": w.q, "q_len": L},
+        "sweep": rows, "linear_fit_ms": {"slope_per_fraction": slope, "intercept": icpt},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -127,6 +280,13 @@ def main():
         sys.exit(2)
 
     w = get_workload(args.workload)
+    if args.threshold is not None:
+        import dataclasses
+        w = dataclasses.replace(w, threshold=args.threshold)
+    if w.steps > 1:
+        return multistep(args, w)
+    if args.sweep:
+        return sweep(args, w)
     select = tuple(int(s) for s in args.select.split(",")) if args.select else w.select
     mask = [1 if j in select else 0 for j in range(w.P)]
     offs = w.offsets
@@ -242,7 +402,7 @@ def main():
                    "fresh_fraction": len(select) / w.P},
         "roofline": {"bound": "mfma", "kernel": "attn_bf16_kernel" if w.dtype == "bf16" else "attn_f32_kernel",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": None},
+                     "traffic": attn_traffic(w, select)},
         "kernels_ms": {"attn_partition_states": {"mean": attn_ms, "median": med(t_attn)},
                        "merge_states": {"mean": merge_ms, "median": med(t_merge)},
                        "contrib": {"mean": mean(t_contrib), "median": med(t_contrib)}},

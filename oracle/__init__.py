@@ -15,6 +15,8 @@ Contents (each function cites the passage of the paper it follows):
   and the ranking / threshold selection used by the planner-driven workload.
 * ``brute``  - the same quantities by pure-Python loops with ``math.exp``,
   for tiny shapes only.
+* ``multistep`` - the planner-driven multi-step workload: per-block state
+  caches across denoising steps, anchor steps and threshold selection.
 
 All pins (what the oracle is checked against besides itself) are in
 ``tests/test_oracle_pins.py``.  The paper's own error-model planner (Alg. 1)

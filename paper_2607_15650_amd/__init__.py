@@ -2,3 +2,4 @@
 context-parallel DiT inference: fresh partition states, state composition and
 contribution weights, as HIP kernels behind a C ABI (include/ditango.h)."""
 from .api import attn_partition_states, merge_states, contrib, contrib_workspace_bytes  # noqa: F401
+from .planner import AnchorPlanner, plan_threshold, rank_partitions  # noqa: F401,E402

@@ -1,0 +1,61 @@
+"""GPU parity of the planner-driven multi-step workload on a reduced shape
+(2 heads, 16,384 tokens, 8 partitions, every query block, 10 steps, anchors
+at steps 0 and 5, threshold 0.05 on the anchor weights): selections, composed
+outputs, LSE and weights against the float64 oracle following the same rule."""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import multistep
+from fixtures import gen_qkv, gen_evolved, get_workload
+
+from helpers import TOL, exact_inputs, max_abs, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def test_planner_workload_reduced():
+    import torch
+    from paper_2607_15650_amd.planner import AnchorPlanner
+    from paper_2607_15650_amd.step import SelectiveAttention
+
+    w = get_workload("planner_bf16_h2_d128_s16384_p8_10steps")
+    x = gen_qkv(w, with_prev=False)
+    steps = [x]
+    for s in range(w.steps - 1):
+        steps.append(gen_evolved(w, steps[-1], s))
+    offs = w.offsets
+    blocks = list(range(w.P))
+
+    sa = SelectiveAttention(w.B, w.H, w.D, offs, w.scale, torch.bfloat16)
+    planners = {qb: AnchorPlanner(w.P, qb, w.anchors, w.threshold) for qb in blocks}
+    gpu = []
+    for s, xs in enumerate(steps):
+        q, k, v = (to_gpu(xs[n], "bf16") for n in ("q", "k", "v"))
+        res = {}
+        for qb in blocks:
+            mask = planners[qb].select(s)
+            out, lse, wp = sa.step(s, qb, q, k, v, mask)
+            wp_h = wp.cpu().numpy()
+            planners[qb].observe(s, wp_h)
+            res[qb] = (mask, out.float().cpu().numpy(), lse.cpu().numpy(), wp_h)
+        gpu.append(res)
+
+    orc = multistep.run([{k: exact_inputs(v, "bf16") for k, v in xs.items()} for xs in steps],
+                        offs, blocks, w.anchors, w.threshold, w.scale)
+    tol = TOL["bf16"]
+    n_reused = 0
+    for s in range(w.steps):
+        for qb in blocks:
+            gm, go, gl, gw = gpu[s][qb]
+            om, oo, ol, ow = orc[s][qb]
+            if gm != om:
+                # allowed only where the anchor weight sits within tolerance of the threshold
+                margin = min(abs(x - w.threshold) for x in orc[max(a for a in w.anchors if a <= s)][qb][3])
+                assert margin <= tol["w"], (s, qb, gm, om, margin)
+                continue
+            n_reused += w.P - sum(gm)
+            assert max_abs(go, oo) <= tol["out"], (s, qb)
+            assert max_abs(gl, ol) <= tol["lse"], (s, qb)
+            assert max_abs(gw, ow) <= tol["w"], (s, qb)
+    assert n_reused > 0          # the run really reused cached states
