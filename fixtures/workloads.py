@@ -113,6 +113,15 @@ _add(Workload(name="planner_bf16_h40_d128_s75600_p8_10steps", dtype="bf16", B=1,
               steps=10, step_noise=0.03, anchors=(0, 5), threshold=0.05))
 
 
+# HunyuanVideo-like shape ([1, 119K, 48, 64]: 129 frames at 720p give a
+# 33 x 45 x 80 latent grid), fresh |j-q| <= 1.
+_add(Workload(name="hunyuan_bf16_h48_d64_s118800_p8", dtype="bf16", B=1, H=48, D=64,
+              grid=(33, 45, 80), P=8, q=3, seed=5, select=(2, 3, 4), prev_noise=0.05))
+# Wan2.1-14B shape with the classifier-free-guidance batch of 2
+# ([2, 76K, 40, 128]), fresh |j-q| <= 1.
+_add(Workload(name="videodit_cfg_bf16_b2_h40_d128_s75600_p8", dtype="bf16", B=2, H=40, D=128,
+              grid=(21, 45, 80), P=8, q=3, seed=6, select=(2, 3, 4), prev_noise=0.05))
+
 # Reduced planner-driven run (same partition structure, 2 heads, 16,384
 # tokens) that the float64 oracle can follow over all steps and blocks.  On
 # these inputs the anchor weights are close to uniform (about 0.12-0.14 for

@@ -101,7 +101,11 @@ ditango_status ditango_attn_partition_states(
  *   out          device, [B][q_len][H][D], dtype `out_dt`.
  *   lse_out      device, [B][H][q_len] float32; may be NULL.
  *   D            head dim: 64 or 128.
- * The output may not overlap any listed input slot.
+ * `out` / `lse_out` may be exactly the first listed slot (same base address,
+ * same dtype): the composition then happens in place, which is how adjacent
+ * group states are folded into one (each output element is written only
+ * after the same element of every listed slot has been read).  Any other
+ * overlap with a listed slot is not allowed.
  */
 ditango_status ditango_merge_states(
     const void* out_states, const float* lse_states, ditango_dtype state_dt,

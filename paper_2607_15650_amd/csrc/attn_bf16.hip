@@ -57,6 +57,10 @@
 #ifndef DITANGO_PIPE
 #define DITANGO_PIPE 1
 #endif
+// Raise the wave priority while it issues the score MFMAs (build-time switch).
+#ifndef DITANGO_PRIO
+#define DITANGO_PRIO 0
+#endif
 
 namespace ditango {
 namespace {
@@ -325,7 +329,13 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
     // barrier
     load_tile(kg, kbuf(i + 1 + C::PF), (i + 1 + C::PF) * BN, true);
     load_tile(vg, vbuf(i + C::PF), (i + C::PF) * BN, false);
+#if DITANGO_PRIO
+    __builtin_amdgcn_s_setprio(1);
+#endif
     qk(k_next, snxt);
+#if DITANGO_PRIO
+    __builtin_amdgcn_s_setprio(0);
+#endif
     bf16x8 pf[QB][C::PS];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {

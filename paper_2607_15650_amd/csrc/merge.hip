@@ -47,7 +47,7 @@ template <> struct Vec8<float> {
   }
 };
 
-constexpr int kMergeThreads = 256;
+constexpr int kMergeThreads = 64;      // small workgroups keep every CU evenly fed
 constexpr int kMergeBatch = 8;    // slots whose loads are in flight together
 
 // Each thread owns one 8-element chunk of one row (row = (b*q_len + r)*H + h,
