@@ -52,6 +52,11 @@ def parse():
                     help="target CPU time of the oracle baseline sample (0 disables it)")
     ap.add_argument("--threshold", type=float, default=None,
                     help="planner-driven workload: anchor-weight threshold (default: the workload's)")
+    ap.add_argument("--planner", choices=("threshold", "error-model"), default="threshold",
+                    help="planner-driven workload: anchor-weight threshold, or the error-model planner "
+                         "(groups of 2, target reuse ratio --reuse, local drift limit --eps-local)")
+    ap.add_argument("--reuse", type=float, default=0.5)
+    ap.add_argument("--eps-local", type=float, default=0.1)
     ap.add_argument("--sweep", action="store_true",
                     help="time the step for each selection of the workload's sweep (long-context workload)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -204,6 +209,61 @@ def multistep(args, w):
     print(json.dumps(res), flush=True)
 
 
+def multistep_error_model(args, w):
+    """Error-model planner (groups of 2) on every query block over w.steps
+    steps: selective time (planning included), all-fresh time, drift."""
+    import numpy as np
+    import torch
+    from fixtures import bf16_bits, gen_qkv, gen_evolved
+    from paper_2607_15650_amd.ase import ErrorModelSelectiveAttention
+    from paper_2607_15650_amd.step import SelectiveAttention
+
+    offs = w.offsets
+    blocks = list(range(w.P))
+    g = lambda a: torch.from_numpy(bf16_bits(a).view(np.int16)).view(torch.bfloat16).cuda()
+    ems = {qb: ErrorModelSelectiveAttention(w.B, w.H, w.D, offs, qb, 2, w.scale, args.reuse, args.eps_local)
+           for qb in blocks}
+    ref = SelectiveAttention(w.B, w.H, w.D, offs, w.scale, torch.bfloat16)
+    x = gen_qkv(w, with_prev=False)
+    t_sel = t_full = 0.0
+    per_step = []
+    n_groups = n_computed = 0
+    for s in range(w.steps):
+        q, k, v = g(x["q"]), g(x["k"]), g(x["v"])
+        torch.cuda.synchronize()
+        anchors, drift = [], []
+        for qb in blocks:
+            t0 = time.perf_counter()
+            out, _, info = ems[qb].step(s, q, k, v)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            fo, _, _ = ref.step(s, qb, q, k, v, [1] * w.P)
+            torch.cuda.synchronize()
+            t2 = time.perf_counter()
+            t_sel += (t1 - t0) * 1e3
+            t_full += (t2 - t1) * 1e3
+            anchors.append(int(info["anchor"]))
+            n_groups += len(ems[qb].groups)
+            n_computed += len(info["compute"])
+            d = out.float() - fo.float()
+            drift.append(float(d.norm() / fo.float().norm()))
+        per_step.append({"step": s, "anchor_blocks": anchors, "drift_rel_l2_max": max(drift)})
+        print(f"[bench] step {s} anchors {anchors} drift {max(drift):.3e}", file=sys.stderr, flush=True)
+        if s + 1 < w.steps:
+            x = gen_evolved(w, x, s)
+    res = {
+        "metric": METRIC, "value": None, "unit": "TFLOP/s", "n_gpus": 1, "steps": w.steps, "warmup": 0,
+        "ms_per_step": t_sel / w.steps, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic (seeded; each step adds 0.03*N(0,1) to Q, K, V)",
+        "config": {"workload": w.name, "planner": "error-model", "groups_of": 2, "reuse_target": args.reuse,
+                   "eps_local": args.eps_local, "query_blocks": len(blocks)},
+        "selective_ms_total": t_sel, "all_fresh_ms_total": t_full, "speedup_vs_all_fresh": t_full / t_sel,
+        "computed_group_fraction": n_computed / n_groups, "per_step": per_step,
+        "note": "wall-clock per block step including the planner's host work and norm read-backs",
+    }
+    print(json.dumps(res), flush=True)
+
+
 def sweep(args, w):
     """Step time for each selection of the workload's sweep (nearest-first sizes)."""
     import numpy as np
@@ -283,6 +343,8 @@ def main():
     if args.threshold is not None:
         import dataclasses
         w = dataclasses.replace(w, threshold=args.threshold)
+    if w.steps > 1 and args.planner == "error-model":
+        return multistep_error_model(args, w)
     if w.steps > 1:
         return multistep(args, w)
     if args.sweep:

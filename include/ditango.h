@@ -138,6 +138,32 @@ ditango_status ditango_contrib(
     int B, int H, int64_t q_len,
     float* w_rows, float* w_part, void* workspace, void* stream);
 
+/*
+ * Bytes of device workspace ditango_state_norms needs for these sizes.
+ */
+size_t ditango_norms_workspace_bytes(int B, int H, int D, int64_t q_len, int n_slots);
+
+/*
+ * Frobenius norms of state outputs, the quantities of the selection
+ * planner's error model (Sec. 4.1.2: the scale ratio alpha(i) =
+ * ||AS(i)|| / ||AS(i_loc)||, Eq. scale_ratio, and the local-state drift that
+ * Eq. error_extrapolation scales by it):
+ *     norms[i] = sqrt( sum over (b, r, h, d) of (OUT_{slots[i]} - REF)^2 )
+ * with REF = 0 when `ref` is NULL.  Reduced in a fixed order: bitwise
+ * identical from run to run.
+ *
+ *   out_states   device, [P][B][q_len][H][D], dtype `dt`.
+ *   slots        host, n_slots int32 indices in [0, P); NULL = all P slots.
+ *   ref          device, [B][q_len][H][D] in dtype `dt`, or NULL.
+ *   norms        device, [n_slots] float32.
+ *   workspace    device, ditango_norms_workspace_bytes(...) bytes, 16-byte
+ *                aligned; its contents on entry do not matter.
+ */
+ditango_status ditango_state_norms(
+    const void* out_states, ditango_dtype dt, int P, const int32_t* slots, int n_slots,
+    int B, int H, int D, int64_t q_len, const void* ref,
+    float* norms, void* workspace, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* ditango_status_string(ditango_status s);
 

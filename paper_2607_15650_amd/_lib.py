@@ -35,6 +35,11 @@ SIGNATURES = {
         _c.c_void_p, _c.c_void_p, _c.c_int,
         _c.c_int, _c.c_int, _c.c_int64,
         _c.c_void_p, _c.c_void_p, _c.c_void_p, _c.c_void_p]),
+    "ditango_norms_workspace_bytes": (_c.c_size_t, [_c.c_int, _c.c_int, _c.c_int, _c.c_int64, _c.c_int]),
+    "ditango_state_norms": (_c.c_int, [
+        _c.c_void_p, _c.c_int, _c.c_int, _c.POINTER(_c.c_int32), _c.c_int,
+        _c.c_int, _c.c_int, _c.c_int, _c.c_int64, _c.c_void_p,
+        _c.c_void_p, _c.c_void_p, _c.c_void_p]),
     "ditango_status_string": (_c.c_char_p, [_c.c_int]),
     "ditango_version": (_c.c_char_p, []),
 }

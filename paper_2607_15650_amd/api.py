@@ -123,3 +123,30 @@ def contrib(lse_states: torch.Tensor, lse_out: torch.Tensor, w_part: torch.Tenso
         w_rows.data_ptr() if w_rows is not None else None, w_part.data_ptr(),
         workspace.data_ptr(), _stream())
     _lib.check("ditango_contrib", st)
+
+
+def norms_workspace_bytes(B: int, H: int, D: int, q_len: int, n_slots: int) -> int:
+    return int(_lib.lib().ditango_norms_workspace_bytes(B, H, D, q_len, n_slots))
+
+
+def state_norms(out_states: torch.Tensor, norms: torch.Tensor, workspace: torch.Tensor,
+                slots: Optional[Sequence[int]] = None, ref: Optional[torch.Tensor] = None) -> None:
+    """norms[i] = ||out_states[slots[i]] - ref||_2 (ditango_state_norms); ref None = 0."""
+    _dev(out_states, norms, workspace, ref)
+    P, B, q_len, H, D = out_states.shape
+    if ref is not None and (tuple(ref.shape) != (B, q_len, H, D) or ref.dtype != out_states.dtype):
+        raise ValueError("ref must be [B, q_len, H, D] in the state dtype")
+    if slots is None:
+        sl, n = None, P
+    else:
+        n = len(slots)
+        sl = (ctypes.c_int32 * n)(*[int(s) for s in slots])
+    if tuple(norms.shape) != (n,) or norms.dtype != torch.float32:
+        raise ValueError("norms must be float32 [n_slots]")
+    need = norms_workspace_bytes(B, H, D, q_len, n)
+    if workspace.numel() * workspace.element_size() < need:
+        raise ValueError(f"workspace too small: need {need} bytes")
+    st = _lib.lib().ditango_state_norms(
+        out_states.data_ptr(), _dtype(out_states), P, sl, n, B, H, D, q_len,
+        ref.data_ptr() if ref is not None else None, norms.data_ptr(), workspace.data_ptr(), _stream())
+    _lib.check("ditango_state_norms", st)

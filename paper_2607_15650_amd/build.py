@@ -16,7 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libditango.so")
-SOURCES = ["ditango_api.cpp", "attn_bf16.hip", "attn_f32.hip", "merge.hip"]
+SOURCES = ["ditango_api.cpp", "attn_bf16.hip", "attn_f32.hip", "merge.hip", "norms.hip"]
 ARCH = "gfx950"
 
 

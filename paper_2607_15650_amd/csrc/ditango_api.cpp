@@ -141,4 +141,48 @@ ditango_status ditango_contrib(
   return from_hip(launch_contrib(a, (hipStream_t)stream));
 }
 
+static int64_t norm_blocks(int B, int H, int D, int64_t q_len) {
+  const int64_t chunks = (int64_t)B * q_len * H * D / 8;
+  return (chunks + kNormChunksPerBlock - 1) / kNormChunksPerBlock;
+}
+
+size_t ditango_norms_workspace_bytes(int B, int H, int D, int64_t q_len, int n_slots) {
+  if (B < 1 || H < 1 || q_len < 1 || n_slots < 1 || (D != 64 && D != 128)) return 0;
+  return (size_t)(norm_blocks(B, H, D, q_len) * n_slots * (int64_t)sizeof(float));
+}
+
+ditango_status ditango_state_norms(
+    const void* out_states, ditango_dtype dt, int P, const int32_t* slots, int n_slots,
+    int B, int H, int D, int64_t q_len, const void* ref,
+    float* norms, void* workspace, void* stream) {
+  if (!out_states || !norms || !workspace) return DITANGO_ERR_INVALID;
+  if (!valid_dtype(dt)) return DITANGO_ERR_INVALID;
+  if (B < 1 || H < 1 || q_len < 1 || P < 1) return DITANGO_ERR_INVALID;
+  if (P > kMaxParts) return DITANGO_ERR_UNSUPPORTED;
+  if (D != 64 && D != 128) return DITANGO_ERR_UNSUPPORTED;
+  if (((uintptr_t)workspace & 15u) != 0) return DITANGO_ERR_INVALID;
+  NormArgs a;
+  memset(&a, 0, sizeof(a));
+  if (slots == nullptr) {
+    n_slots = P;
+    for (int j = 0; j < P; ++j) a.slots[j] = j;
+  } else {
+    if (n_slots < 1 || n_slots > kMaxParts) return DITANGO_ERR_INVALID;
+    for (int j = 0; j < n_slots; ++j) {
+      if (slots[j] < 0 || slots[j] >= P) return DITANGO_ERR_INVALID;
+      a.slots[j] = slots[j];
+    }
+  }
+  const int64_t nb = norm_blocks(B, H, D, q_len);
+  if (nb > 0x7fffffffLL) return DITANGO_ERR_UNSUPPORTED;
+  a.states = out_states;
+  a.ref = ref;
+  a.norms = norms;
+  a.partial = (float*)workspace;
+  a.elems = (int64_t)B * q_len * H * D;
+  a.n = n_slots;
+  a.blocks = (int)nb;
+  return from_hip(launch_norms(a, dt, (hipStream_t)stream));
+}
+
 }  // extern "C"

@@ -52,6 +52,20 @@ struct ContribArgs {
   int n_blocks;
 };
 
+struct NormArgs {
+  const void* states;       // [P][elems]
+  const void* ref;          // [elems] or null
+  float* norms;             // [n]
+  float* partial;           // workspace [n][blocks]
+  int64_t elems;            // B*q_len*H*D (a multiple of 8)
+  int n;
+  int blocks;               // workgroups per slot
+  int32_t slots[kMaxParts];
+};
+
+constexpr int kNormThreads = 256;
+constexpr int kNormChunksPerBlock = kNormThreads * 16;   // 8-element chunks per workgroup
+
 // Rows of the composed-LSE array one contrib workgroup reduces.
 constexpr int kContribThreads = 256;
 constexpr int kContribRowsPerThread = 8;
@@ -62,6 +76,7 @@ hipError_t launch_attn_f32(const AttnArgs& a, int D, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, ditango_dtype sdt, ditango_dtype odt, int D,
                         hipStream_t s);
 hipError_t launch_contrib(const ContribArgs& a, hipStream_t s);
+hipError_t launch_norms(const NormArgs& a, ditango_dtype dt, hipStream_t s);
 
 // Workgroup index remap for the 8 XCDs of the chip: hardware hands out
 // consecutive workgroup ids round-robin over the XCDs, so id b runs on XCD

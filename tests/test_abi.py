@@ -116,3 +116,18 @@ def test_contrib_workspace_size(L):
     assert f(1, 40, 9450, 8) == ((40 * 9450 + 2047) // 2048) * 8 * 4
     assert f(0, 1, 1, 1) == 0
     assert f(1, 1, 1, 1) == 4
+
+
+def test_state_norms_argument_validation(L):
+    f = L.ditango_state_norms
+    assert f(None, 1, 4, None, 0, 1, 2, 64, 8, None, FAKE, FAKE, None) == 1
+    assert f(FAKE, 1, 4, None, 0, 1, 2, 64, 8, None, None, FAKE, None) == 1
+    assert f(FAKE, 1, 4, None, 0, 1, 2, 64, 8, None, FAKE, None, None) == 1
+    assert f(FAKE, 9, 4, None, 0, 1, 2, 64, 8, None, FAKE, FAKE, None) == 1
+    assert f(FAKE, 1, 0, None, 0, 1, 2, 64, 8, None, FAKE, FAKE, None) == 1
+    assert f(FAKE, 1, 65, None, 0, 1, 2, 64, 8, None, FAKE, FAKE, None) == 2
+    assert f(FAKE, 1, 4, None, 0, 1, 2, 96, 8, None, FAKE, FAKE, None) == 2
+    assert f(FAKE, 1, 4, None, 0, 1, 2, 64, 8, None, FAKE, FAKE + 8, None) == 1
+    bad = (ctypes.c_int32 * 2)(0, 4)
+    assert f(FAKE, 1, 4, bad, 2, 1, 2, 64, 8, None, FAKE, FAKE, None) == 1
+    assert L.ditango_norms_workspace_bytes(1, 40, 128, 9450, 8) == ((40 * 9450 * 128 // 8 + 4095) // 4096) * 8 * 4

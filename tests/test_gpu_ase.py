@@ -1,0 +1,75 @@
+"""GPU parity of the error-model selection (Alg. 1 with group states) on the
+reduced planner workload: state norms against float64, then per step the
+anchor decision, the computed groups and the composed output against the
+float64 oracle following the same rule (decisions compared exactly unless the
+oracle's margin to a threshold is within 2 %)."""
+import numpy as np
+import pytest
+
+from oracle import ase_planner
+from fixtures import gen_qkv, gen_evolved, get_workload
+
+from helpers import TOL, exact_inputs, max_abs, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+G, R, EPS_LOCAL = 2, 0.75, 0.085   # decision margins of this run stay above 1 %
+
+
+def test_state_norms_against_float64():
+    import torch
+    from paper_2607_15650_amd import api
+    rng = np.random.default_rng(5)
+    P, B, L, H, D = 5, 2, 301, 3, 64
+    x = rng.standard_normal((P, B, L, H, D)).astype(np.float32)
+    ref = rng.standard_normal((B, L, H, D)).astype(np.float32)
+    for dt in ("bf16", "f32"):
+        st, rf = to_gpu(x, dt), to_gpu(ref, dt)
+        X, RF = exact_inputs(x, dt), exact_inputs(ref, dt)
+        ws = torch.empty(api.norms_workspace_bytes(B, H, D, L, P), dtype=torch.uint8, device="cuda")
+        n = torch.empty(3, dtype=torch.float32, device="cuda")
+        api.state_norms(st, n, ws, slots=[4, 0, 2], ref=rf)
+        n2 = torch.empty(P, dtype=torch.float32, device="cuda")
+        api.state_norms(st, n2, ws)
+        torch.cuda.synchronize()
+        exp = [np.linalg.norm(X[j] - RF) for j in (4, 0, 2)]
+        np.testing.assert_allclose(n.cpu().numpy(), exp, rtol=1e-5)
+        np.testing.assert_allclose(n2.cpu().numpy(), [np.linalg.norm(X[j]) for j in range(P)], rtol=1e-5)
+
+
+def test_error_model_planner_reduced():
+    import torch
+    from paper_2607_15650_amd.ase import ErrorModelSelectiveAttention
+
+    w = get_workload("planner_bf16_h2_d128_s16384_p8_10steps")
+    x = gen_qkv(w, with_prev=False)
+    steps = [x]
+    for s in range(w.steps - 1):
+        steps.append(gen_evolved(w, steps[-1], s))
+    offs = w.offsets
+    tol = TOL["bf16"]
+    reused_total = 0
+    for qb in (3, 6):
+        em = ErrorModelSelectiveAttention(w.B, w.H, w.D, offs, qb, G, w.scale, R, EPS_LOCAL, torch.bfloat16)
+        gpu = []
+        for t, xs in enumerate(steps):
+            q, k, v = (to_gpu(xs[n], "bf16") for n in ("q", "k", "v"))
+            out, lse, info = em.step(t, q, k, v)
+            gpu.append((info["anchor"], list(info["compute"]), out.float().cpu().numpy(), lse.cpu().numpy()))
+        orc = ase_planner.run([{n: exact_inputs(v_, "bf16") for n, v_ in xs.items()} for xs in steps],
+                              offs, qb, G, R, EPS_LOCAL, w.scale)
+        for t in range(w.steps):
+            ga, gc, go, gl = gpu[t]
+            o = orc[t]
+            if (ga, gc) != (o["anchor"], o["compute"]):
+                eps = o["eps"]
+                # the group whose ASE defines eps (the quantile) decides identically on both sides
+                margins = [abs(v_ - eps) / max(eps, 1e-30) for v_ in o["ase"].values() if v_ != eps]
+                if o["drift"] is not None:
+                    margins.append(abs(o["drift"] - EPS_LOCAL) / EPS_LOCAL)
+                assert min(margins) <= 0.02, (qb, t, ga, gc, o["anchor"], o["compute"], min(margins))
+                break
+            reused_total += len(em.groups) - len(gc)
+            assert max_abs(go, o["out"]) <= tol["out"], (qb, t)
+            assert max_abs(gl, o["lse"]) <= tol["lse"], (qb, t)
+    assert reused_total > 0

@@ -53,3 +53,16 @@ def test_oracle_multistep_reuse_semantics_tiny():
                 assert mask == [1] * P
             else:
                 assert mask == oracle.plan_threshold(res[0][qb][3], qb, 0.3)
+
+
+def test_quantile_rule_matches_oracle():
+    from paper_2607_15650_amd.ase import quantile_r
+    from oracle.ase_planner import r_quantile
+    rng = np.random.default_rng(3)
+    for _ in range(300):
+        v = list(rng.random(int(rng.integers(1, 20))))
+        r = float(rng.random())
+        assert quantile_r(v, r) == r_quantile(v, r)
+    assert quantile_r([3.0, 1.0, 2.0, 4.0], 0.5) == 2.0
+    assert quantile_r([3.0, 1.0, 2.0, 4.0], 0.75) == 3.0
+    assert quantile_r([3.0], 0.1) == 3.0
