@@ -37,8 +37,8 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE (each scaled so that a plain 1 GiB
 # elementwise copy reads / writes 1 GiB), keyed by the SHA-256 prefix of the
 # kernel source they were taken on; reported only while the source matches.
-ATTN_TRAFFIC = {"src_sha256_16": "6416ca39a158485f", "workload": "videodit_bf16_h40_d128_s75600_p8",
-                "fetch_bytes": 759960 * 1024 * 2.0, "write_bytes": 314640 * 1024 * 1.0}
+ATTN_TRAFFIC = {"src_sha256_16": "40d3a0cb784fab6c", "workload": "videodit_bf16_h40_d128_s75600_p8",
+                "fetch_bytes": 746644.875 * 1024 * 2.0, "write_bytes": 288103.9375 * 1024 * 1.0}
 
 
 def parse():
@@ -139,6 +139,36 @@ def cpu_baseline(w, x, select, target_s):
         cores = 1
     per_step_s = t * w.q_len / n
     return n, t, per_step_s, cores
+
+
+def device_reference(torch):
+    """What library kernels reach on this GPU in the same process, as context
+    for the roofline fractions (clocks and power limits vary from card to
+    card): a large bf16 GEMM through torch.matmul and a 1 GiB device copy."""
+    def timed(fn, it):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(it):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / it
+    n = 8192
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    c = torch.empty(n, n, device="cuda", dtype=torch.bfloat16)
+    gemm_ms = timed(lambda: torch.matmul(a, b, out=c), 10)
+    del a, b, c
+    src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    copy_ms = timed(lambda: dst.copy_(src), 10)
+    del src, dst
+    return {"bf16_gemm_8192_tflops": 2 * n ** 3 / (gemm_ms * 1e-3) / 1e12,
+            "copy_1gib_gbs": 2 * (1 << 30) / (copy_ms * 1e-3) / 1e9}
 
 
 def multistep(args, w):
@@ -438,6 +468,8 @@ def main():
     achieved = flops / (attn_ms * 1e-3) / 1e12
     merge_gbs = merge_bytes / (merge_ms * 1e-3) / 1e9
 
+    ref = device_reference(torch)
+
     cpu = None
     if args.cpu_seconds > 0:
         print("[bench] timing the CPU oracle baseline", file=sys.stderr, flush=True)
@@ -471,6 +503,7 @@ def main():
         "merge_roofline": {"bound": "hbm", "achieved": merge_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                            "frac": merge_gbs / PEAK_HBM_GBS, "bytes_per_launch": merge_bytes},
         "attn_tflops_per_step_flops": flops / 1e12,
+        "device_reference": ref,
         "cpu_baseline": cpu,
         "input_gen_s": t_gen,
     }

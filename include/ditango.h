@@ -70,7 +70,8 @@ typedef enum {
  *   q, k, v      device; dtype `dt`; Q [B][q_len][H][D], K and V [B][S][H][D]
  *                with S = kv_offsets[P].
  *   dt           DITANGO_BF16 or DITANGO_F32 (inputs, states share it).
- *   D            head dim: 64 or 128.
+ *   D            head dim: 64 or 128; H*D at most 65536
+ *                (DITANGO_ERR_UNSUPPORTED beyond).
  *   kv_offsets   host, P+1 int64, kv_offsets[0] = 0, non-decreasing.
  *   select       host, P bytes; non-zero = compute partition j fresh.
  *   scale        softmax scale applied to q.k (normally 1/sqrt(D)).

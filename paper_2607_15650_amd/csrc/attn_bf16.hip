@@ -48,19 +48,12 @@
 //   row i = 8*(r/4) + 4*(l/32) + (r%4), column j = l % 32.
 #include "internal.h"
 
-// Explicit instruction interleave hints in the main loop (build-time switch).
-#ifndef DITANGO_SCHED
-#define DITANGO_SCHED 0
-#endif
 // Software-pipelined main loop (scores of tile i+1 beside the softmax of
 // tile i) or the sequential one (build-time switch).
 #ifndef DITANGO_PIPE
 #define DITANGO_PIPE 1
 #endif
-// Raise the wave priority while it issues the score MFMAs (build-time switch).
-#ifndef DITANGO_PRIO
-#define DITANGO_PRIO 0
-#endif
+
 
 namespace ditango {
 namespace {
@@ -90,17 +83,21 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-// 16-byte direct load global -> LDS for the wave: lane l's 16 bytes from `src`
-// land at LDS byte lds_base + 16*l.  Issued from inline assembly so that the
-// compiler does not order every later LDS read of this wave after it (it
-// cannot tell the DMA target apart from the tiles being read); completion is
-// awaited explicitly with s_waitcnt vmcnt before the workgroup barrier that
-// publishes the tile.
-__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_base) {
-  const uint32_t base = __builtin_amdgcn_readfirstlane(lds_base);   // wave-uniform
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+// 16-byte direct load global -> LDS for the wave: lane l's 16 bytes from
+// base + voff land at LDS byte lds_base + 16*l.  `base` and `lds_base` are
+// wave-uniform (scalar registers), `voff` is the lane's byte offset.  Issued
+// from inline assembly so that the compiler does not order every later LDS
+// read of this wave after it (it cannot tell the DMA target apart from the
+// tiles being read); completion is awaited explicitly with s_waitcnt vmcnt
+// before the workgroup barrier that publishes the tile.
+__device__ __forceinline__ void lds_dma16(const void* base, uint32_t voff, uint32_t lds_base) {
+  const uint64_t p = (uint64_t)(uintptr_t)base;
+  const uint64_t sbase = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32)) << 32) |
+                         (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p);
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_base);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
                :
-               : "v"(src), "s"(base)
+               : "v"(voff), "s"(sbase), "s"(m0v)
                : "memory", "m0");
 }
 
@@ -209,25 +206,49 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
 
   // ---- direct global -> LDS tile loads.  Lane l of a 1 KiB load writes LDS
   // unit l of that KiB, i.e. row l / UNITS, stored unit l % UNITS; it fetches
-  // the global unit that the swizzle maps there.  Rows past the end of the
-  // partition are clamped to its last key: their scores are masked to -inf and
-  // their probabilities are exactly 0, so any finite value will do, and every
-  // load stays inside the partition.
+  // the global unit that the swizzle maps there.  The lane's byte offset from
+  // the tile's first key is the same for every tile, so it is computed once;
+  // the tile base is wave-uniform.  Rows past the end of the partition are
+  // clamped to its last key: their scores are masked to -inf and their
+  // probabilities are exactly 0, so any finite value will do, and every load
+  // stays inside the partition.
   const int last_key = kv_len > 0 ? kv_len - 1 : 0;
   const int ld_row = lane / C::UNITS;
   const int ld_unit = lane % C::UNITS;
-  auto load_tile = [&](const __bf16* src, unsigned char* dst, int key0, bool is_k) {
+  const uint32_t row_bytes = (uint32_t)HD * 2;
+  uint32_t ld_off_k[C::LOADS_W], ld_off_v[C::LOADS_W];
 #pragma unroll
-    for (int i = 0; i < C::LOADS_W; ++i) {
-      const int li = wave * C::LOADS_W + i;               // which KiB of the tile
-      const int row = li * C::ROWS_PER_LOAD + ld_row;     // tile row (key)
-      const int key = min(key0 + row, last_key);
-      const int unit = ld_unit ^ (is_k ? swz_k<D>(row) : swz_v<D>(row));
-      lds_dma16(src + (int64_t)key * HD + unit * 8, lds_addr(dst + li * 1024));
+  for (int i = 0; i < C::LOADS_W; ++i) {
+    const int row = (wave * C::LOADS_W + i) * C::ROWS_PER_LOAD + ld_row;   // tile row (key)
+    ld_off_k[i] = row * row_bytes + (uint32_t)((ld_unit ^ swz_k<D>(row)) * 16);
+    ld_off_v[i] = row * row_bytes + (uint32_t)((ld_unit ^ swz_v<D>(row)) * 16);
+  }
+  const uint32_t smem_lds = lds_addr(smem);
+  auto load_tile = [&](const __bf16* src, uint32_t dst, int key0, bool is_k) {
+    if (key0 + BN <= kv_len) {
+      const __bf16* base = src + (int64_t)key0 * HD;
+#pragma unroll
+      for (int i = 0; i < C::LOADS_W; ++i)
+        lds_dma16(base, is_k ? ld_off_k[i] : ld_off_v[i], dst + (wave * C::LOADS_W + i) * 1024);
+    } else {
+      // the partition's last tile (or one past its end): clamp every row
+      const int key_b = min(key0, last_key);
+      const __bf16* base = src + (int64_t)key_b * HD;
+#pragma unroll
+      for (int i = 0; i < C::LOADS_W; ++i) {
+        const int li = wave * C::LOADS_W + i;
+        const int row = li * C::ROWS_PER_LOAD + ld_row;
+        const int key = min(key0 + row, last_key) - key_b;
+        const int unit = ld_unit ^ (is_k ? swz_k<D>(row) : swz_v<D>(row));
+        lds_dma16(base, (uint32_t)key * row_bytes + (uint32_t)(unit * 16), dst + li * 1024);
+      }
     }
   };
 
-  // rings of NBUF K tiles and NBUF V tiles: tile t lives in slot t % NBUF
+  // rings of NBUF K tiles and NBUF V tiles (LDS byte addresses): tile t lives
+  // in slot t % NBUF
+  auto kbuf_lds = [&](int t) { return smem_lds + (uint32_t)((t & (NBUF - 1)) * C::TILEB); };
+  auto vbuf_lds = [&](int t) { return smem_lds + (uint32_t)((NBUF + (t & (NBUF - 1))) * C::TILEB); };
   auto kbuf = [&](int t) { return smem + (t & (NBUF - 1)) * C::TILEB; };
   auto vbuf = [&](int t) { return smem + (NBUF + (t & (NBUF - 1))) * C::TILEB; };
 
@@ -327,15 +348,9 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
     // K_{i+1+PF} and V_{i+PF} land in LDS during the next PF iterations; they
     // overwrite K_{i+1+PF-NBUF} and V_{i+PF-NBUF}, consumed before the last
     // barrier
-    load_tile(kg, kbuf(i + 1 + C::PF), (i + 1 + C::PF) * BN, true);
-    load_tile(vg, vbuf(i + C::PF), (i + C::PF) * BN, false);
-#if DITANGO_PRIO
-    __builtin_amdgcn_s_setprio(1);
-#endif
+    load_tile(kg, kbuf_lds(i + 1 + C::PF), (i + 1 + C::PF) * BN, true);
+    load_tile(vg, vbuf_lds(i + C::PF), (i + C::PF) * BN, false);
     qk(k_next, snxt);
-#if DITANGO_PRIO
-    __builtin_amdgcn_s_setprio(0);
-#endif
     bf16x8 pf[QB][C::PS];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -365,25 +380,6 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
         for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma32(va, pf[qb][s], o[qb][db]);
       }
     }
-#if DITANGO_SCHED
-    // Interleave (one scheduling region): the QK^T MFMAs of tile i+1, each
-    // beside one K-operand LDS read, two FMAs and two exp2 of tile i; then
-    // the PV MFMAs, each beside two transpose reads and the VALU work of the
-    // row sums, bf16 conversion and the row maximum of tile i+1.
-#pragma unroll
-    for (int k = 0; k < C::KB * C::KS * QB; ++k) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);   // VALU
-      __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);   // transcendental
-    }
-#pragma unroll
-    for (int k = 0; k < C::PS * C::DB * QB; ++k) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // DS read
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // VALU
-    }
-#endif
     float alpha[QB];
     if (update_max(snxt, alpha, has_next)) {
 #pragma unroll
@@ -403,11 +399,11 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   if (n_tiles > 0) {
     // K_0, then the loads iterations -PF..-1 would have issued, in the same
     // order as the loop issues them
-    load_tile(kg, kbuf(0), 0, true);
+    load_tile(kg, kbuf_lds(0), 0, true);
 #pragma unroll
     for (int j = -C::PF; j < 0; ++j) {
-      load_tile(kg, kbuf(j + 1 + C::PF), (j + 1 + C::PF) * BN, true);
-      load_tile(vg, vbuf(j + C::PF), (j + C::PF) * BN, false);
+      load_tile(kg, kbuf_lds(j + 1 + C::PF), (j + 1 + C::PF) * BN, true);
+      load_tile(vg, vbuf_lds(j + C::PF), (j + C::PF) * BN, false);
     }
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_0, K_1, V_0 have landed
     __syncthreads();
@@ -427,14 +423,14 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   if (n_tiles > 0) {
 #pragma unroll
     for (int j = -C::PF; j < 0; ++j) {
-      load_tile(kg, kbuf(j + C::PF), (j + C::PF) * BN, true);
-      load_tile(vg, vbuf(j + C::PF), (j + C::PF) * BN, false);
+      load_tile(kg, kbuf_lds(j + C::PF), (j + C::PF) * BN, true);
+      load_tile(vg, vbuf_lds(j + C::PF), (j + C::PF) * BN, false);
     }
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_0, V_0 have landed
     __syncthreads();
     for (int i = 0; i < n_tiles; ++i) {
-      load_tile(kg, kbuf(i + C::PF), (i + C::PF) * BN, true);
-      load_tile(vg, vbuf(i + C::PF), (i + C::PF) * BN, false);
+      load_tile(kg, kbuf_lds(i + C::PF), (i + C::PF) * BN, true);
+      load_tile(vg, vbuf_lds(i + C::PF), (i + C::PF) * BN, false);
       f32x16 sc[C::KB][QB];
       qk(kbuf(i), sc);
       if ((i + 1) * BN > kv_len) mask_tail(sc, i * BN);
@@ -462,7 +458,7 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
             pf[qb][2 * kb + hh] = __builtin_convertvector(x, bf16x8);
           }
         l[qb] += ls;
-      }
+        }
       const unsigned char* v_cur = vbuf(i);
 #pragma unroll
       for (int s = 0; s < C::PS; ++s) {

@@ -49,6 +49,9 @@ ditango_status ditango_attn_partition_states(
   // row indices of a query tile and element offsets stay in int64; the
   // per-partition key count must fit int32 (checked above), so must q_len.
   if (q_len > 0x7fffffffLL) return DITANGO_ERR_UNSUPPORTED;
+  // the bf16 kernel addresses a key tile with 32-bit lane offsets from its
+  // first row: H*D <= 65536 keeps a 128-key tile within 16 MiB
+  if ((int64_t)H * D > 65536) return DITANGO_ERR_UNSUPPORTED;
 
   AttnArgs a;
   memset(&a, 0, sizeof(a));

@@ -66,6 +66,8 @@ def test_attn_argument_validation(L):
     assert attn(L, q_len=-3) == 1
     assert attn(L, D=96) == 2
     assert attn(L, D=256) == 2
+    assert attn(L, H=513, D=128) == 2                     # H*D beyond 65536
+    assert attn(L, H=1025, D=64) == 2
     assert attn(L, offs=(0, 6, 5), sel=(1, 1)) == 1       # decreasing offsets
     assert attn(L, offs=(1, 6, 10), sel=(1, 1)) == 1      # offsets[0] != 0
     assert attn(L, scale=float("nan")) == 1
