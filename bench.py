@@ -35,10 +35,11 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 
 # HBM bytes per launch of the attention kernel at the default workload, from
 # rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE (each scaled so that a plain 1 GiB
-# elementwise copy reads / writes 1 GiB), keyed by the SHA-256 prefix of the
-# kernel source they were taken on; reported only while the source matches.
-ATTN_TRAFFIC = {"src_sha256_16": "40d3a0cb784fab6c", "workload": "videodit_bf16_h40_d128_s75600_p8",
-                "fetch_bytes": 746644.875 * 1024 * 2.0, "write_bytes": 288103.9375 * 1024 * 1.0}
+# elementwise copy reads / writes 1 GiB), keyed by the build id (source and
+# compile options) of the kernel they were taken on; reported only while the
+# build id matches.
+ATTN_TRAFFIC = {"build_id": "3c28cce0327fe541", "workload": "videodit_bf16_h40_d128_s75600_p8",
+                "fetch_bytes": 746620 * 1024 * 2.0, "write_bytes": 287956 * 1024 * 1.0}
 
 
 def parse():
@@ -78,16 +79,13 @@ def algorithmic(w, select):
 
 
 def attn_traffic(w, select):
-    """Profiled HBM bytes per attention launch, or None when the kernel source,
+    """Profiled HBM bytes per attention launch, or None when the kernel build,
     the workload or the selection differs from the one the counters were
     taken on."""
-    import hashlib
-    src = os.path.join(ROOT, "paper_2607_15650_amd", "csrc", "attn_bf16.hip")
-    try:
-        h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    except OSError:
+    from paper_2607_15650_amd import build
+    if build.source_id("attn_bf16.hip") != ATTN_TRAFFIC["build_id"]:
         return None
-    if h != ATTN_TRAFFIC["src_sha256_16"] or w.name != ATTN_TRAFFIC["workload"] or tuple(select) != w.select:
+    if w.name != ATTN_TRAFFIC["workload"] or tuple(select) != w.select:
         return None
     return ATTN_TRAFFIC["fetch_bytes"] + ATTN_TRAFFIC["write_bytes"]
 
@@ -142,9 +140,11 @@ def cpu_baseline(w, x, select, target_s):
 
 
 def device_reference(torch):
-    """What library kernels reach on this GPU in the same process, as context
-    for the roofline fractions (clocks and power limits vary from card to
-    card): a large bf16 GEMM through torch.matmul and a 1 GiB device copy."""
+    """What this GPU sustains, measured in the same process, as context for
+    the roofline fractions (clocks and power limits vary from card to card):
+    a stream of independent bf16 MFMAs filling the chip (the library's probe
+    kernel), a large bf16 GEMM through torch.matmul and a 1 GiB device copy."""
+    from paper_2607_15650_amd import api
     def timed(fn, it):
         for _ in range(2):
             fn()
@@ -157,6 +157,14 @@ def device_reference(torch):
         e1.record()
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / it
+    n_wg = 2 * torch.cuda.get_device_properties(0).multi_processor_count
+    sink = torch.empty(n_wg * 256, dtype=torch.float32, device="cuda")
+    probe_flops = [0.0]
+
+    def probe():
+        probe_flops[0] = api.probe_mfma_bf16(n_wg, 20000, sink)
+    probe_ms = timed(probe, 5)
+    del sink
     n = 8192
     a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
     b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
@@ -167,7 +175,8 @@ def device_reference(torch):
     dst = torch.empty_like(src)
     copy_ms = timed(lambda: dst.copy_(src), 10)
     del src, dst
-    return {"bf16_gemm_8192_tflops": 2 * n ** 3 / (gemm_ms * 1e-3) / 1e12,
+    return {"bf16_mfma_probe_tflops": probe_flops[0] / (probe_ms * 1e-3) / 1e12,
+            "bf16_gemm_8192_tflops": 2 * n ** 3 / (gemm_ms * 1e-3) / 1e12,
             "copy_1gib_gbs": 2 * (1 << 30) / (copy_ms * 1e-3) / 1e9}
 
 
@@ -468,7 +477,25 @@ def main():
     achieved = flops / (attn_ms * 1e-3) / 1e12
     merge_gbs = merge_bytes / (merge_ms * 1e-3) / 1e9
 
+    # pass 3: the merge alone with a cold cache (a 1 GiB write before each
+    # launch evicts the states from L2 and the 256 MB Infinity Cache)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    t_cold = []
+    for i in range(max(3, min(args.steps, 10))):
+        flush.fill_(float(i))
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        api.merge_states(out_states, lse_states, out, lse)
+        e1.record()
+        torch.cuda.synchronize()
+        t_cold.append(e0.elapsed_time(e1))
+    del flush
+    merge_cold_ms = mean(t_cold)
+
     ref = device_reference(torch)
+    if w.dtype == "bf16":
+        ref["attn_frac_of_probe"] = achieved / ref["bf16_mfma_probe_tflops"]
 
     cpu = None
     if args.cpu_seconds > 0:
@@ -501,7 +528,10 @@ def main():
                        "merge_states": {"mean": merge_ms, "median": med(t_merge)},
                        "contrib": {"mean": mean(t_contrib), "median": med(t_contrib)}},
         "merge_roofline": {"bound": "hbm", "achieved": merge_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                           "frac": merge_gbs / PEAK_HBM_GBS, "bytes_per_launch": merge_bytes},
+                           "frac": merge_gbs / PEAK_HBM_GBS, "bytes_per_launch": merge_bytes,
+                           "cold_cache": {"ms": merge_cold_ms,
+                                          "achieved": merge_bytes / (merge_cold_ms * 1e-3) / 1e9,
+                                          "frac": merge_bytes / (merge_cold_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}},
         "attn_tflops_per_step_flops": flops / 1e12,
         "device_reference": ref,
         "cpu_baseline": cpu,

@@ -165,6 +165,22 @@ ditango_status ditango_state_norms(
     int B, int H, int D, int64_t q_len, const void* ref,
     float* norms, void* workspace, void* stream);
 
+/*
+ * Device characterisation, not part of the method: the dense bf16 MFMA rate
+ * the GPU sustains at the clock it runs at under MFMA load, to hold the
+ * attention kernel against beside the published peak.  Launches
+ * n_workgroups workgroups of 256 threads (4 waves); every wave issues `iters`
+ * rounds of four independent 32x32x16 bf16 MFMAs and nothing else, so one
+ * call performs n_workgroups * 4 * iters * 4 * 32768 flops.  Time it with
+ * events on `stream`.
+ *
+ *   n_workgroups  1 .. 1048576 (use several per compute unit).
+ *   iters         1 .. 1048576.
+ *   sink          device, n_workgroups * 256 float32; receives one value per
+ *                 thread that keeps the products live (meaningless otherwise).
+ */
+ditango_status ditango_probe_mfma_bf16(int n_workgroups, int iters, float* sink, void* stream);
+
 /* Static, NUL-terminated description of a status code. */
 const char* ditango_status_string(ditango_status s);
 

@@ -40,6 +40,7 @@ SIGNATURES = {
         _c.c_void_p, _c.c_int, _c.c_int, _c.POINTER(_c.c_int32), _c.c_int,
         _c.c_int, _c.c_int, _c.c_int, _c.c_int64, _c.c_void_p,
         _c.c_void_p, _c.c_void_p, _c.c_void_p]),
+    "ditango_probe_mfma_bf16": (_c.c_int, [_c.c_int, _c.c_int, _c.c_void_p, _c.c_void_p]),
     "ditango_status_string": (_c.c_char_p, [_c.c_int]),
     "ditango_version": (_c.c_char_p, []),
 }

@@ -150,3 +150,15 @@ def state_norms(out_states: torch.Tensor, norms: torch.Tensor, workspace: torch.
         out_states.data_ptr(), _dtype(out_states), P, sl, n, B, H, D, q_len,
         ref.data_ptr() if ref is not None else None, norms.data_ptr(), workspace.data_ptr(), _stream())
     _lib.check("ditango_state_norms", st)
+
+
+def probe_mfma_bf16(n_workgroups: int, iters: int, sink: torch.Tensor) -> float:
+    """Enqueue the MFMA-rate probe (ditango_probe_mfma_bf16) on the current
+    stream; returns the flops the launch performs.  ``sink`` is a float32
+    device tensor of at least n_workgroups * 256 elements."""
+    _dev(sink)
+    if sink.dtype != torch.float32 or sink.numel() < n_workgroups * 256:
+        raise ValueError("sink must be float32 with n_workgroups * 256 elements")
+    st = _lib.lib().ditango_probe_mfma_bf16(n_workgroups, iters, sink.data_ptr(), _stream())
+    _lib.check("ditango_probe_mfma_bf16", st)
+    return float(n_workgroups) * 4 * iters * 4 * 32768

@@ -188,4 +188,10 @@ ditango_status ditango_state_norms(
   return from_hip(launch_norms(a, dt, (hipStream_t)stream));
 }
 
+ditango_status ditango_probe_mfma_bf16(int n_workgroups, int iters, float* sink, void* stream) {
+  if (!sink || n_workgroups < 1 || iters < 1) return DITANGO_ERR_INVALID;
+  if (n_workgroups > (1 << 20) || iters > (1 << 20)) return DITANGO_ERR_INVALID;
+  return from_hip(launch_probe_mfma(n_workgroups, iters, sink, (hipStream_t)stream));
+}
+
 }  // extern "C"

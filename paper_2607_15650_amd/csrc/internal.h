@@ -78,6 +78,9 @@ hipError_t launch_merge(const MergeArgs& a, ditango_dtype sdt, ditango_dtype odt
 hipError_t launch_contrib(const ContribArgs& a, hipStream_t s);
 hipError_t launch_norms(const NormArgs& a, ditango_dtype dt, hipStream_t s);
 
+constexpr int kProbeThreads = 256;   // 4 waves per workgroup
+hipError_t launch_probe_mfma(int n_workgroups, int iters, float* sink, hipStream_t s);
+
 // Workgroup index remap for the 8 XCDs of the chip: hardware hands out
 // consecutive workgroup ids round-robin over the XCDs, so id b runs on XCD
 // b % 8.  The remap gives every XCD a contiguous run of logical task ids, so

@@ -14,7 +14,7 @@ HEADER = os.path.join(ROOT, "include", "ditango.h")
 def header_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(ditango_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(ditango_[a-z0-9_]+)\s*\(", text)))
 
 
 @pytest.fixture(scope="module")
@@ -133,3 +133,12 @@ def test_state_norms_argument_validation(L):
     bad = (ctypes.c_int32 * 2)(0, 4)
     assert f(FAKE, 1, 4, bad, 2, 1, 2, 64, 8, None, FAKE, FAKE, None) == 1
     assert L.ditango_norms_workspace_bytes(1, 40, 128, 9450, 8) == ((40 * 9450 * 128 // 8 + 4095) // 4096) * 8 * 4
+
+
+def test_probe_argument_validation(L):
+    f = L.ditango_probe_mfma_bf16
+    assert f(0, 10, FAKE, None) == 1
+    assert f(4, 0, FAKE, None) == 1
+    assert f(4, 10, None, None) == 1
+    assert f((1 << 20) + 1, 10, FAKE, None) == 1
+    assert f(4, (1 << 20) + 1, FAKE, None) == 1
