@@ -35,24 +35,24 @@
 //
 // Pipeline
 //   Iteration i computes the scores of tile i+1 (MFMA) in the same basic block
-//   as the exponentials of tile i (VALU), then accumulates P_i V_i (MFMA)
-//   beside the row maximum of tile i+1 (VALU), so each block has both kinds of
-//   work for the scheduler to interleave.  The loads of K_{i+2} and V_{i+1}
-//   are in flight during the whole iteration.  The running maximum is raised
-//   only when a tile's maximum exceeds it by more than 2^8, so the output
-//   accumulator is rescaled on a handful of tiles only (probabilities stay
-//   below 2^8; the final normalisation divides the same factor out of OUT and
-//   the row sum).
+//   as the exponentials of tile i (VALU), then accumulates P_i V_i (MFMA).
+//   The loads of K_{i+2} and V_{i+1} are in flight during the whole
+//   iteration.
+//
+// Running maximum
+//   No per-tile row maximum is taken.  Probabilities are computed against the
+//   running maximum m as it stands; only a tile whose probabilities grow past
+//   2^40 (scores more than 40 above m, base 2, or the first tile, where m is
+//   still -inf) is redone after raising m to the tile's row maximum and
+//   rescaling the accumulators.  Floating point keeps the relative precision
+//   of the large probabilities, and the final normalisation divides the same
+//   factor out of OUT and the row sum, so the result does not depend on how
+//   far m lags the true maximum.
 //
 // Accumulator layout of the 32x32 MFMA (lane l, register r):
 //   row i = 8*(r/4) + 4*(l/32) + (r%4), column j = l % 32.
 #include "internal.h"
 
-// Software-pipelined main loop (scores of tile i+1 beside the softmax of
-// tile i) or the sequential one (build-time switch).
-#ifndef DITANGO_PIPE
-#define DITANGO_PIPE 1
-#endif
 
 
 namespace ditango {
@@ -308,42 +308,72 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   };
 
   const float sl2 = a.scale_log2;
-  constexpr float kLazy = 8.0f;
-  // Row maximum of a score tile (scaled, base 2) and the lazy update of the
-  // running maximum m: m moves only when the tile maximum exceeds it by more
-  // than kLazy.  Returns whether any lane of the wave moved its m; alpha gets
-  // the factor exp2(m_old - m_new) that rescales O and l.
-  auto update_max = [&](f32x16 (&sc)[C::KB][QB], float (&alpha)[QB], bool valid) {
-    bool grow = false;
+  // Probabilities are taken against a running maximum m that is raised only
+  // when a tile's probabilities grow large: exp2(s*scale*log2e - m) for every
+  // score of the tile, with this lane's partial row sums in ls.
+  auto softmax_tile = [&](const f32x16 (&sc)[C::KB][QB], bf16x8 (&pf)[QB][C::PS], float (&ls)[QB]) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      float mx = -INFINITY;
+      float sum = 0.f;
 #pragma unroll
       for (int kb = 0; kb < C::KB; ++kb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][qb][r]);
-      mx = pair_max(mx) * sl2;
-      const float mnew = (valid && mx > m[qb] + kLazy) ? mx : m[qb];
-      alpha[qb] = fast_exp2(m[qb] - mnew);
-      grow |= mnew != m[qb];
-      m[qb] = mnew;
-      l[qb] *= alpha[qb];
+        for (int hh = 0; hh < 2; ++hh) {
+          f32x8 x;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            x[e] = fast_exp2(__builtin_fmaf(sc[kb][qb][8 * hh + e], sl2, -m[qb]));
+            sum += x[e];
+          }
+          pf[qb][2 * kb + hh] = __builtin_convertvector(x, bf16x8);
+        }
+      ls[qb] = sum;
     }
-    return __builtin_amdgcn_ballot_w64(grow) != 0;
+  };
+  // A tile whose probabilities against m sum past 2^40 in some lane (its
+  // scores exceed m by more than 40, base 2), or hold an inf or a NaN (the
+  // first tile: m = -inf), is redone: m is raised to the row maximum of the
+  // tile, O and l are rescaled, and the probabilities recomputed.  Otherwise
+  // probabilities stay below 2^40 and the row sum below 2^40 times the key
+  // count, well inside float32; OUT = O / l and LSE = m + log2 l do not
+  // depend on which m was used.  So no tile maximum is taken in the common
+  // case.
+  constexpr float kBig = 1099511627776.0f;   // 2^40
+  auto softmax_checked = [&](const f32x16 (&sc)[C::KB][QB], bf16x8 (&pf)[QB][C::PS]) {
+    float ls[QB];
+    softmax_tile(sc, pf, ls);
+    bool big = false;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) big |= !(ls[qb] <= kBig);
+    if (__builtin_amdgcn_ballot_w64(big) != 0) {
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < C::KB; ++kb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][qb][r]);
+        const float mnew = fmaxf(m[qb], pair_max(mx) * sl2);
+        const float alpha = m[qb] == -INFINITY ? 0.f : fast_exp2(m[qb] - mnew);
+        m[qb] = mnew;
+        l[qb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) o[qb][db] *= alpha;
+      }
+      softmax_tile(sc, pf, ls);
+    }
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) l[qb] += ls[qb];
   };
 
   // One pipelined iteration over key tile i.  On entry S_i holds the scores
-  // of tile i, the running maximum already covers them, and O, l are scaled
-  // to it.  Block A: the MFMAs of S_{i+1} = K_{i+1} Q^T run while the VALU
+  // of tile i.  Block A: the MFMAs of S_{i+1} = K_{i+1} Q^T run while the VALU
   // turns S_i into probabilities P_i (exp2, row sums, bf16).  Block B: the
-  // MFMAs of O += V_i P_i run while the VALU takes the row maximum of S_{i+1}.
+  // MFMAs of O += V_i P_i.
   auto iteration = [&](int i, f32x16 (&scur)[C::KB][QB], f32x16 (&snxt)[C::KB][QB]) {
     const unsigned char* k_next = kbuf(i + 1);
     const unsigned char* v_cur = vbuf(i);
     // Tile i is the partition's last and partial: mask its keys past the end.
-    // The masking waits until here so that the maximum taken in the previous
-    // iteration could sit beside the PV MFMAs; it is unaffected, because the
-    // rows past the end repeat the last key, which is in this tile.
     if ((i + 1) * BN > kv_len) mask_tail(scur, i * BN);
     // K_{i+1+PF} and V_{i+PF} land in LDS during the next PF iterations; they
     // overwrite K_{i+1+PF-NBUF} and V_{i+PF-NBUF}, consumed before the last
@@ -352,40 +382,22 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
     load_tile(vg, vbuf_lds(i + C::PF), (i + C::PF) * BN, false);
     qk(k_next, snxt);
     bf16x8 pf[QB][C::PS];
+    softmax_checked(scur, pf);
+    // O^T += V^T P^T; the V operands of key step s+1 are read while the
+    // MFMAs of step s run
+    bf16x8 va[2][C::DB];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      float ls = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < C::KB; ++kb)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          f32x8 x;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            x[e] = fast_exp2(__builtin_fmaf(scur[kb][qb][8 * hh + e], sl2, -m[qb]));
-            ls += x[e];
-          }
-          pf[qb][2 * kb + hh] = __builtin_convertvector(x, bf16x8);
-        }
-      l[qb] += ls;
-    }
-    const bool has_next = (i + 1) * BN < kv_len;
-    // O^T += V^T P^T
+    for (int db = 0; db < C::DB; ++db) va[0][db] = v_frag(v_cur, 0, db);
 #pragma unroll
     for (int s = 0; s < C::PS; ++s) {
+      if (s + 1 < C::PS) {
 #pragma unroll
-      for (int db = 0; db < C::DB; ++db) {
-        const bf16x8 va = v_frag(v_cur, s, db);
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma32(va, pf[qb][s], o[qb][db]);
+        for (int db = 0; db < C::DB; ++db) va[(s + 1) & 1][db] = v_frag(v_cur, s + 1, db);
       }
-    }
-    float alpha[QB];
-    if (update_max(snxt, alpha, has_next)) {
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
+      for (int db = 0; db < C::DB; ++db)
 #pragma unroll
-        for (int db = 0; db < C::DB; ++db) o[qb][db] *= alpha[qb];
+        for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma32(va[s & 1][db], pf[qb][s], o[qb][db]);
     }
     // K_{i+2} and V_{i+1}, used by the next iteration, have landed for this
     // wave; the barrier makes that true for the whole workgroup
@@ -394,7 +406,6 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   };
 
   const int n_tiles = (kv_len + BN - 1) / BN;
-#if DITANGO_PIPE
   f32x16 s0[C::KB][QB], s1[C::KB][QB];
   if (n_tiles > 0) {
     // K_0, then the loads iterations -PF..-1 would have issued, in the same
@@ -408,73 +419,12 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_0, K_1, V_0 have landed
     __syncthreads();
     qk(kbuf(0), s0);
-    float alpha0[QB];
-    update_max(s0, alpha0, true);          // O and l are still zero
-    __syncthreads();
     // K_i is consumed one iteration early (scores of the next tile)
     for (int i = 0; i < n_tiles; i += 2) {
       iteration(i, s0, s1);
       if (i + 1 < n_tiles) iteration(i + 1, s1, s0);
     }
   }
-#else
-  // Sequential form: each iteration takes the scores, softmax and PV of one
-  // tile; the two waves sharing a SIMD overlap each other's phases.
-  if (n_tiles > 0) {
-#pragma unroll
-    for (int j = -C::PF; j < 0; ++j) {
-      load_tile(kg, kbuf_lds(j + C::PF), (j + C::PF) * BN, true);
-      load_tile(vg, vbuf_lds(j + C::PF), (j + C::PF) * BN, false);
-    }
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_0, V_0 have landed
-    __syncthreads();
-    for (int i = 0; i < n_tiles; ++i) {
-      load_tile(kg, kbuf_lds(i + C::PF), (i + C::PF) * BN, true);
-      load_tile(vg, vbuf_lds(i + C::PF), (i + C::PF) * BN, false);
-      f32x16 sc[C::KB][QB];
-      qk(kbuf(i), sc);
-      if ((i + 1) * BN > kv_len) mask_tail(sc, i * BN);
-      float alpha[QB];
-      if (update_max(sc, alpha, true)) {
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-          for (int db = 0; db < C::DB; ++db) o[qb][db] *= alpha[qb];
-      }
-      bf16x8 pf[QB][C::PS];
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        float ls = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < C::KB; ++kb)
-#pragma unroll
-          for (int hh = 0; hh < 2; ++hh) {
-            f32x8 x;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              x[e] = fast_exp2(__builtin_fmaf(sc[kb][qb][8 * hh + e], sl2, -m[qb]));
-              ls += x[e];
-            }
-            pf[qb][2 * kb + hh] = __builtin_convertvector(x, bf16x8);
-          }
-        l[qb] += ls;
-        }
-      const unsigned char* v_cur = vbuf(i);
-#pragma unroll
-      for (int s = 0; s < C::PS; ++s) {
-#pragma unroll
-        for (int db = 0; db < C::DB; ++db) {
-          const bf16x8 va = v_frag(v_cur, s, db);
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma32(va, pf[qb][s], o[qb][db]);
-        }
-      }
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_{i+1}, V_{i+1} have landed
-      __syncthreads();
-    }
-  }
-#endif
-
 
   // ---- epilogue: normalise, write OUT_j and LSE_j of slot j
   __bf16* outg = (__bf16*)a.out_states;

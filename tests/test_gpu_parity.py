@@ -232,6 +232,54 @@ def test_ragged_shapes(dtype, D, H, q_len, lens):
     assert max_abs(lse.cpu().numpy(), ml) <= tol["lse"]
 
 
+@pytest.mark.parametrize("D", [128, 64])
+def test_running_max_far_below_and_above(D):
+    """Score ranges that force the kernel to raise its running maximum in the
+    middle of a partition: per head, the key norms ramp up along the sequence
+    (later tiles score far above the first one, up to overflow of exp2
+    against a stale maximum), ramp down (later tiles underflow against the
+    first), or jump once.  Queries scaled by 32 make scores span hundreds, so
+    against the first tile's maximum exp2 would overflow float32.  Such rows
+    are nearly one-hot, where the bf16 rounding of the probabilities bounds
+    the OUT error by 2^-8 max|v| (+ 2^-9 |OUT| for the bf16 store); V is
+    scaled by 1/4 to keep that bound (0.0065 here) under the 1e-2 tolerance,
+    which is stated for unit-variance V."""
+    import torch
+    a = api()
+    rng = np.random.default_rng(99 + D)
+    B, H, q_len, dtype = 1, 3, 300, "bf16"
+    lens = [1000, 130]
+    S = sum(lens)
+    offs = [0, lens[0], S]
+    q = rng.standard_normal((B, q_len, H, D), dtype=np.float32) * 32.0
+    k = rng.standard_normal((B, S, H, D), dtype=np.float32)
+    ramp = np.linspace(0.05, 1.0, S, dtype=np.float32)
+    k[:, :, 0, :] *= ramp[None, :, None]                        # rising
+    k[:, :, 1, :] *= ramp[::-1][None, :, None]                  # falling
+    k[:, :, 2, :] *= np.where(np.arange(S) < 400, 0.05, 1.0).astype(np.float32)[None, :, None]   # jump
+    v = rng.standard_normal((B, S, H, D), dtype=np.float32) * 0.25
+    scale = 1 / math.sqrt(D)
+    P = len(lens)
+    out_states, lse_states = new_state_cache(P, B, q_len, H, D, dtype)
+    a.attn_partition_states(to_gpu(q, dtype), to_gpu(k, dtype), to_gpu(v, dtype), offs, [1] * P, scale,
+                            out_states, lse_states)
+    torch.cuda.synchronize()
+    Q, K, V = (exact_inputs(t, dtype) for t in (q, k, v))
+    outs, lses = oracle.partition_states(Q, K, V, offs, scale)
+    for j in range(P):
+        go = out_states[j].float().cpu().numpy()
+        gl = lse_states[j].cpu().numpy()
+        assert np.all(np.isfinite(go)) and np.all(np.isfinite(gl)), j
+        assert max_abs(go, outs[j]) <= TOL[dtype]["out"], j
+        assert max_abs(gl, lses[j]) <= TOL[dtype]["lse"], j
+    # premise: in some row, the partition's top score exceeds the first 64-key
+    # tile's top score by more than 128 (base 2): exp2 against the first
+    # tile's maximum overflows float32 there
+    sc = np.einsum("bqhd,bkhd->bhqk", Q, K[:, :lens[0]]) * scale
+    gap = (sc.max(axis=3) - sc[..., :64].max(axis=3)) / math.log(2.0)
+    assert gap.max() > 128.0, gap.max()
+
+
 def test_unselected_slots_untouched_bitwise():
     import torch
     a = api()
