@@ -89,6 +89,20 @@ ditango_status ditango_attn_partition_states(
     void* out_states, float* lse_states, void* stream);
 
 /*
+ * The same with the state dtype chosen separately: bf16 inputs may keep
+ * their states in float32 (the states at full precision; the composed
+ * output of ditango_merge_states may still be bf16).  `out_states` is
+ * [P][B][q_len][H][D] in `state_dt`.  state_dt must equal dt, or be
+ * DITANGO_F32 with dt = DITANGO_BF16 (DITANGO_ERR_UNSUPPORTED otherwise).
+ * ditango_attn_partition_states(...) is this call with state_dt = dt.
+ */
+ditango_status ditango_attn_partition_states_ex(
+    const void* q, const void* k, const void* v, ditango_dtype dt,
+    int B, int H, int D, int64_t q_len,
+    const int64_t* kv_offsets, int P, const uint8_t* select, float scale,
+    void* out_states, ditango_dtype state_dt, float* lse_states, void* stream);
+
+/*
  * Composition of cached and fresh states (Sec. 2.2.4, Eq. composition, n-ary):
  *     M = max_j LSE_j,  LSE = M + log sum_j exp(LSE_j - M),
  *     OUT = sum_j exp(LSE_j - LSE) * OUT_j

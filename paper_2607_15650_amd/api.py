@@ -52,7 +52,9 @@ def attn_partition_states(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
                           offsets: Sequence[int], select: Sequence[int], scale: float,
                           out_states: torch.Tensor, lse_states: torch.Tensor) -> None:
     """Fresh states of the selected partitions into their slots
-    (ditango_attn_partition_states).  Unselected slots are left untouched."""
+    (ditango_attn_partition_states).  Unselected slots are left untouched.
+    ``out_states`` is in the input dtype, or float32 for bf16 inputs
+    (ditango_attn_partition_states_ex: states at full precision)."""
     _dev(q, k, v, out_states, lse_states)
     B, q_len, H, D = q.shape
     P = len(offsets) - 1
@@ -62,18 +64,27 @@ def attn_partition_states(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
         raise ValueError("k/v shape mismatch")
     if k.shape[1] != offsets[-1]:
         raise ValueError("offsets[-1] must equal the key/value sequence length")
-    if tuple(out_states.shape) != (P, B, q_len, H, D) or out_states.dtype != q.dtype:
-        raise ValueError("out_states must be [P, B, q_len, H, D] in the input dtype")
+    if tuple(out_states.shape) != (P, B, q_len, H, D):
+        raise ValueError("out_states must be [P, B, q_len, H, D]")
+    if out_states.dtype != q.dtype and not (q.dtype == torch.bfloat16 and out_states.dtype == torch.float32):
+        raise ValueError("out_states must be in the input dtype, or float32 for bf16 inputs")
     if tuple(lse_states.shape) != (P, B, H, q_len) or lse_states.dtype != torch.float32:
         raise ValueError("lse_states must be float32 [P, B, H, q_len]")
     if k.dtype != q.dtype or v.dtype != q.dtype:
         raise ValueError("q, k, v must share a dtype")
     offs = (ctypes.c_int64 * (P + 1))(*[int(x) for x in offsets])
     sel = (ctypes.c_uint8 * P)(*[1 if s else 0 for s in select])
-    st = _lib.lib().ditango_attn_partition_states(
-        q.data_ptr(), k.data_ptr(), v.data_ptr(), _dtype(q), B, H, D, q_len,
-        offs, P, sel, float(scale), out_states.data_ptr(), lse_states.data_ptr(), _stream())
-    _lib.check("ditango_attn_partition_states", st)
+    if out_states.dtype == q.dtype:
+        st = _lib.lib().ditango_attn_partition_states(
+            q.data_ptr(), k.data_ptr(), v.data_ptr(), _dtype(q), B, H, D, q_len,
+            offs, P, sel, float(scale), out_states.data_ptr(), lse_states.data_ptr(), _stream())
+        _lib.check("ditango_attn_partition_states", st)
+    else:
+        st = _lib.lib().ditango_attn_partition_states_ex(
+            q.data_ptr(), k.data_ptr(), v.data_ptr(), _dtype(q), B, H, D, q_len,
+            offs, P, sel, float(scale), out_states.data_ptr(), _dtype(out_states), lse_states.data_ptr(),
+            _stream())
+        _lib.check("ditango_attn_partition_states_ex", st)
 
 
 def merge_states(out_states: torch.Tensor, lse_states: torch.Tensor, out: torch.Tensor,

@@ -149,7 +149,13 @@ template <int D> __device__ __forceinline__ int swz_v(int key) {
 // this wave are outstanding (expcnt and lgkmcnt not waited for)
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | 0x0F70; }
 
-template <int D, int QB, int NW, int BN, int NBUF, int WPE>
+// four consecutive output elements of a state row, in the state type
+__device__ __forceinline__ void store4(__bf16* p, const f32x4& x) {
+  *(bf16x4*)p = __builtin_convertvector(x, bf16x4);
+}
+__device__ __forceinline__ void store4(float* p, const f32x4& x) { *(f32x4*)p = x; }
+
+template <int D, int QB, int NW, int BN, int NBUF, int WPE, typename TS>
 __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs a) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];   // 2*NBUF tiles
@@ -427,7 +433,7 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   }
 
   // ---- epilogue: normalise, write OUT_j and LSE_j of slot j
-  __bf16* outg = (__bf16*)a.out_states;
+  TS* outg = (TS*)a.out_states;
   const int64_t slot_elems = (int64_t)a.B * a.q_len * HD;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
@@ -435,7 +441,7 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
     const int64_t row = row0 + qb * 32 + lr;
     if (row < a.q_len) {
       const float inv = lt > 0.f ? 1.0f / lt : 0.f;
-      __bf16* dst = outg + (int64_t)slot * slot_elems + ((int64_t)b * a.q_len + row) * HD +
+      TS* dst = outg + (int64_t)slot * slot_elems + ((int64_t)b * a.q_len + row) * HD +
                     (int64_t)h * D + 4 * g;
 #pragma unroll
       for (int db = 0; db < C::DB; ++db)
@@ -444,7 +450,7 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
           f32x4 x;
 #pragma unroll
           for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
-          *(bf16x4*)(dst + db * 32 + 8 * r4) = __builtin_convertvector(x, bf16x4);
+          store4(dst + db * 32 + 8 * r4, x);
         }
       if (g == 0) {
         const float lse = lt > 0.f ? (m[qb] + __builtin_amdgcn_logf(lt)) * kLn2 : -INFINITY;
@@ -454,12 +460,12 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   }
 }
 
-template <int D, int QB, int NW, int BN, int NBUF, int WPE>
+template <int D, int QB, int NW, int BN, int NBUF, int WPE, typename TS>
 hipError_t launch_cfg(const AttnArgs& a0, hipStream_t s) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
   const size_t lds = (size_t)2 * NBUF * C::TILEB;
   static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE>,
+      (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, TS>,
       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (attr != hipSuccess) return attr;
   AttnArgs a = a0;
@@ -467,7 +473,8 @@ hipError_t launch_cfg(const AttnArgs& a0, hipStream_t s) {
   const int64_t nblk = (int64_t)a.q_tiles * a.H * a.B * a.n_sel;
   if (nblk <= 0) return hipSuccess;
   if (nblk > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE>), dim3((unsigned)nblk), dim3(C::NT), lds, s, a);
+  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, TS>), dim3((unsigned)nblk), dim3(C::NT), lds,
+                     s, a);
   return hipGetLastError();
 }
 
@@ -483,9 +490,11 @@ hipError_t launch_cfg(const AttnArgs& a0, hipStream_t s) {
 #define DITANGO_D64_CFG 1, 8, 64, 2, 2
 #endif
 
-hipError_t launch_attn_bf16(const AttnArgs& a, int D, hipStream_t s) {
-  if (D == 128) return launch_cfg<128, DITANGO_D128_CFG>(a, s);
-  if (D == 64) return launch_cfg<64, DITANGO_D64_CFG>(a, s);
+hipError_t launch_attn_bf16(const AttnArgs& a, int D, bool state_f32, hipStream_t s) {
+  if (D == 128)
+    return state_f32 ? launch_cfg<128, DITANGO_D128_CFG, float>(a, s) : launch_cfg<128, DITANGO_D128_CFG, __bf16>(a, s);
+  if (D == 64)
+    return state_f32 ? launch_cfg<64, DITANGO_D64_CFG, float>(a, s) : launch_cfg<64, DITANGO_D64_CFG, __bf16>(a, s);
   return hipErrorInvalidValue;
 }
 

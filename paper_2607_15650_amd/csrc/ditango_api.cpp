@@ -30,13 +30,14 @@ const char* ditango_status_string(ditango_status s) {
 
 const char* ditango_version(void) { return "0.1.0"; }
 
-ditango_status ditango_attn_partition_states(
+ditango_status ditango_attn_partition_states_ex(
     const void* q, const void* k, const void* v, ditango_dtype dt,
     int B, int H, int D, int64_t q_len,
     const int64_t* kv_offsets, int P, const uint8_t* select, float scale,
-    void* out_states, float* lse_states, void* stream) {
+    void* out_states, ditango_dtype state_dt, float* lse_states, void* stream) {
   if (!q || !k || !v || !kv_offsets || !select || !out_states || !lse_states) return DITANGO_ERR_INVALID;
-  if (!valid_dtype(dt)) return DITANGO_ERR_INVALID;
+  if (!valid_dtype(dt) || !valid_dtype(state_dt)) return DITANGO_ERR_INVALID;
+  if (state_dt != dt && !(dt == DITANGO_BF16 && state_dt == DITANGO_F32)) return DITANGO_ERR_UNSUPPORTED;
   if (B < 1 || H < 1 || q_len < 1 || P < 1) return DITANGO_ERR_INVALID;
   if (P > kMaxParts) return DITANGO_ERR_UNSUPPORTED;
   if (D != 64 && D != 128) return DITANGO_ERR_UNSUPPORTED;
@@ -76,8 +77,17 @@ ditango_status ditango_attn_partition_states(
   a.n_sel = n;
   if (n == 0) return DITANGO_OK;
   hipStream_t s = (hipStream_t)stream;
-  if (dt == DITANGO_BF16) return from_hip(launch_attn_bf16(a, D, s));
+  if (dt == DITANGO_BF16) return from_hip(launch_attn_bf16(a, D, state_dt == DITANGO_F32, s));
   return from_hip(launch_attn_f32(a, D, s));
+}
+
+ditango_status ditango_attn_partition_states(
+    const void* q, const void* k, const void* v, ditango_dtype dt,
+    int B, int H, int D, int64_t q_len,
+    const int64_t* kv_offsets, int P, const uint8_t* select, float scale,
+    void* out_states, float* lse_states, void* stream) {
+  return ditango_attn_partition_states_ex(q, k, v, dt, B, H, D, q_len, kv_offsets, P, select, scale,
+                                          out_states, dt, lse_states, stream);
 }
 
 ditango_status ditango_merge_states(

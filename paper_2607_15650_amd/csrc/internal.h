@@ -16,7 +16,7 @@ struct AttnArgs {
   const void* q;            // [B][q_len][H][D]
   const void* k;            // [B][S][H][D]
   const void* v;            // [B][S][H][D]
-  void* out_states;         // [P][B][q_len][H][D]
+  void* out_states;         // [P][B][q_len][H][D], state dtype
   float* lse_states;        // [P][B][H][q_len]
   int64_t q_len;
   int64_t S;
@@ -71,7 +71,8 @@ constexpr int kContribThreads = 256;
 constexpr int kContribRowsPerThread = 8;
 constexpr int kContribRowsPerBlock = kContribThreads * kContribRowsPerThread;
 
-hipError_t launch_attn_bf16(const AttnArgs& a, int D, hipStream_t s);
+// bf16 inputs; states in bf16, or in float32 when state_f32
+hipError_t launch_attn_bf16(const AttnArgs& a, int D, bool state_f32, hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, int D, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, ditango_dtype sdt, ditango_dtype odt, int D,
                         hipStream_t s);

@@ -30,16 +30,20 @@ class SelectiveAttention:
     """Runs fresh-state / compose / weights steps for a set of query blocks.
 
     ``offsets`` are the P+1 token offsets of the partitions; query block i is
-    partition i of the same sequence.
+    partition i of the same sequence.  ``state_dtype`` is the dtype of the
+    cached states: the input dtype (default) or float32 for bf16 inputs; the
+    composed output is in the input dtype either way.
     """
 
     def __init__(self, B: int, H: int, D: int, offsets: Sequence[int], scale: float,
-                 dtype: torch.dtype = torch.bfloat16, device="cuda"):
+                 dtype: torch.dtype = torch.bfloat16, device="cuda",
+                 state_dtype: torch.dtype = None):
         self.B, self.H, self.D = B, H, D
         self.offsets = [int(o) for o in offsets]
         self.P = len(self.offsets) - 1
         self.scale = float(scale)
         self.dtype = dtype
+        self.state_dtype = state_dtype if state_dtype is not None else dtype
         self.device = device
         self.caches = {}
         self._ws = {}
@@ -47,7 +51,7 @@ class SelectiveAttention:
     def cache(self, qb: int) -> StateCache:
         if qb not in self.caches:
             L = self.offsets[qb + 1] - self.offsets[qb]
-            self.caches[qb] = StateCache(self.P, self.B, L, self.H, self.D, self.dtype, self.device)
+            self.caches[qb] = StateCache(self.P, self.B, L, self.H, self.D, self.state_dtype, self.device)
         return self.caches[qb]
 
     def step(self, step: int, qb: int, q_all: torch.Tensor, k: torch.Tensor, v: torch.Tensor,

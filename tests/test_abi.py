@@ -142,3 +142,14 @@ def test_probe_argument_validation(L):
     assert f(4, 10, None, None) == 1
     assert f((1 << 20) + 1, 10, FAKE, None) == 1
     assert f(4, (1 << 20) + 1, FAKE, None) == 1
+
+
+def test_attn_ex_state_dtype_validation(L):
+    f = L.ditango_attn_partition_states_ex
+    o = (ctypes.c_int64 * 3)(0, 5, 10)
+    s = (ctypes.c_uint8 * 2)(1, 1)
+    call = lambda dt, sdt: f(FAKE, FAKE, FAKE, dt, 1, 2, 128, 10, o, 2, s, 0.1, FAKE, sdt, FAKE, None)
+    assert call(1, 7) == 1            # unknown state dtype
+    assert call(0, 1) == 2            # float32 inputs with bf16 states: not built
+    o_bad = (ctypes.c_int64 * 3)(0, 6, 5)
+    assert f(FAKE, FAKE, FAKE, 1, 1, 2, 128, 10, o_bad, 2, s, 0.1, FAKE, 0, FAKE, None) == 1

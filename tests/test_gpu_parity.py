@@ -280,6 +280,52 @@ def test_running_max_far_below_and_above(D):
     assert gap.max() > 128.0, gap.max()
 
 
+@pytest.mark.parametrize("D", [128, 64])
+def test_fp32_states_for_bf16_inputs(D):
+    """bf16 inputs with the states kept in float32 (the _ex entry point): the
+    states match the oracle, differ from the bf16 states by the bf16 store
+    rounding only, and compose into a bf16 or a float32 output."""
+    import torch
+    a = api()
+    rng = np.random.default_rng(5 + D)
+    B, H, q_len, lens = 1, 4, 333, [150, 0, 449, 64]
+    S = sum(lens)
+    offs = [0]
+    for n in lens:
+        offs.append(offs[-1] + n)
+    P = len(lens)
+    q = rng.standard_normal((B, q_len, H, D), dtype=np.float32)
+    k = rng.standard_normal((B, S, H, D), dtype=np.float32) + 0.2
+    v = rng.standard_normal((B, S, H, D), dtype=np.float32)
+    scale = 1 / math.sqrt(D)
+    qg, kg, vg = (to_gpu(t, "bf16") for t in (q, k, v))
+    st32, ls32 = new_state_cache(P, B, q_len, H, D, "f32")
+    st16, ls16 = new_state_cache(P, B, q_len, H, D, "bf16")
+    a.attn_partition_states(qg, kg, vg, offs, [1] * P, scale, st32, ls32)
+    a.attn_partition_states(qg, kg, vg, offs, [1] * P, scale, st16, ls16)
+    out16 = torch.empty((B, q_len, H, D), dtype=torch.bfloat16, device="cuda")
+    out32 = torch.empty((B, q_len, H, D), dtype=torch.float32, device="cuda")
+    lse = torch.empty((B, H, q_len), dtype=torch.float32, device="cuda")
+    a.merge_states(st32, ls32, out16, lse)
+    a.merge_states(st32, ls32, out32, None)
+    torch.cuda.synchronize()
+    assert st32.dtype == torch.float32
+    Q, K, V = (exact_inputs(t, "bf16") for t in (q, k, v))
+    outs, lses = oracle.partition_states(Q, K, V, offs, scale)
+    g32 = st32.cpu().numpy()
+    g16 = st16.float().cpu().numpy()
+    for j in range(P):
+        assert max_abs(g32[j], outs[j]) <= TOL["bf16"]["out"], j
+        assert max_abs(ls32[j].cpu().numpy(), lses[j]) <= TOL["bf16"]["lse"], j
+        # same kernel arithmetic: the bf16 states are the float32 ones rounded
+        assert np.all(np.abs(g16[j] - g32[j]) <= np.abs(g32[j]) * 2.0 ** -8 + 1e-30), j
+        assert np.array_equal(ls32[j].cpu().numpy(), ls16[j].cpu().numpy()), j
+    mo, ml = oracle.merge(outs, lses)
+    assert max_abs(out16.float().cpu().numpy(), mo) <= TOL["bf16"]["out"]
+    assert max_abs(out32.cpu().numpy(), mo) <= TOL["bf16"]["out"]
+    assert max_abs(lse.cpu().numpy(), ml) <= TOL["bf16"]["lse"]
+
+
 def test_unselected_slots_untouched_bitwise():
     import torch
     a = api()
