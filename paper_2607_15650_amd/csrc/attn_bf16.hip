@@ -425,6 +425,8 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_0, K_1, V_0 have landed
     __syncthreads();
     qk(kbuf(0), s0);
+    // every wave has read K_0 before iteration 0 loads K_2 into its slot
+    __syncthreads();
     // K_i is consumed one iteration early (scores of the next tile)
     for (int i = 0; i < n_tiles; i += 2) {
       iteration(i, s0, s1);

@@ -5,7 +5,7 @@
 // over a list of cached/fresh state slots.  Pure streaming: every OUT slot is
 // read once and the output written once, so the kernel is bound by HBM
 // bandwidth.  The state loads are issued first; the weights of a row are
-// reduced across the lanes that own the row while they are in flight.
+// formed while they are in flight.
 //
 // contrib: per-row weights W_j = e^{LSE_j - LSE} (w_i of Sec. 4.1.1; the
 // anchor weights of Eq. lse_weight) and their mean over all rows per
@@ -53,17 +53,15 @@ constexpr int kMergeBatch = 8;    // slots whose loads are in flight together
 // Each thread owns one 8-element chunk of one row (row = (b*q_len + r)*H + h,
 // rows contiguous in every slot), so the CPR = D/8 lanes of a row are
 // consecutive lanes of one wave.  The thread first issues the state loads of
-// the first batch of slots; lane k of the row loads LSE_j for j = k, k+CPR, ...
-// at the same time.  The row's maximum, log-sum-exp and weights are then
-// reduced across its CPR lanes with shuffles (no LDS, no barrier), and every
-// lane forms OUT = sum_j w_j OUT_j in float32.
+// the first batch of slots, then the loads of the row's LSEs; it forms the
+// row's maximum, log-sum-exp and weights itself (no cross-lane exchange, no
+// LDS, no barrier) and OUT = sum_j w_j OUT_j in float32.
 // NS > 0: the slot count is the compile-time constant NS (the common
 // partition counts get their own instantiation, free of run-time loop bounds);
 // NS == 0: any count up to kMaxParts, read from the arguments.
 template <typename TS, typename TO, int D, int NS>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a) {
   constexpr int CPR = D / 8;                      // chunks (lanes) per row
-  constexpr int LPL = ((NS > 0 ? NS : kMaxParts) + CPR - 1) / CPR;   // LSEs per lane
   const int n = NS > 0 ? NS : a.n;
   const int64_t c = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x;
   const bool live = c < a.rows * CPR;
@@ -81,46 +79,42 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   const int h = (int)(row % a.H);
   const int64_t br = row / a.H;
   const int64_t li = ((br / a.q_len) * a.H + h) * a.q_len + br % a.q_len;
-  float lv[LPL];
+  // every lane of the row loads all the row's LSEs (the row's lanes share
+  // the addresses, so each load instruction touches one line per row) and
+  // forms the weights itself: no cross-lane exchange
+  constexpr int NL = NS > 0 ? NS : kMaxParts;
+  float lv[NL];
   float mx = -INFINITY;
 #pragma unroll
-  for (int k = 0; k < LPL; ++k) {
-    const int j = ch + k * CPR;
-    lv[k] = (live && j < n) ? a.lse[(int64_t)a.slots[j] * lse_slot + li] : -INFINITY;
-    mx = fmaxf(mx, lv[k]);
+  for (int j = 0; j < NL; ++j) {
+    lv[j] = (live && j < n) ? a.lse[(int64_t)a.slots[j] * lse_slot + li] : -INFINITY;
+    mx = fmaxf(mx, lv[j]);
   }
-#pragma unroll
-  for (int off = CPR / 2; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, CPR));
   float tot = 0.f;
 #pragma unroll
-  for (int k = 0; k < LPL; ++k) {
-    lv[k] = mx == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((lv[k] - mx) * kLog2e);
-    tot += lv[k];
+  for (int j = 0; j < NL; ++j) {
+    lv[j] = mx == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((lv[j] - mx) * kLog2e);
+    tot += lv[j];
   }
-#pragma unroll
-  for (int off = CPR / 2; off > 0; off >>= 1) tot += __shfl_xor(tot, off, CPR);
   const float inv = tot > 0.f ? 1.0f / tot : 0.f;
   const float lse = tot > 0.f ? mx + __builtin_amdgcn_logf(tot) * kLn2 : -INFINITY;
-
-  // weight of slot j sits in lane j % CPR of the row, entry j / CPR
-  auto weight = [&](int j) {
-    float v = lv[0];
-#pragma unroll
-    for (int k = 1; k < LPL; ++k)
-      if (j / CPR == k) v = lv[k];
-    return __shfl(v, j % CPR, CPR) * inv;
-  };
+  auto weight = [&](int j) { return lv[j] * inv; };
   f32x8 acc = f32x8{};
 #pragma unroll
   for (int u = 0; u < kMergeBatch; ++u)
     if (u < n) acc += weight(u) * x[u];
-  for (int j0 = kMergeBatch; j0 < n; j0 += kMergeBatch) {
+  // later batches: fully unrolled over the largest slot count so that every
+  // weight index is a compile-time constant (the weights stay in registers)
 #pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u)
-      x[u] = (live && j0 + u < n) ? Vec8<TS>::load(st + (int64_t)a.slots[j0 + u] * slot_elems) : f32x8{};
+  for (int j0 = kMergeBatch; j0 < NL; j0 += kMergeBatch) {
+    if (j0 < n) {
 #pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u)
-      if (j0 + u < n) acc += weight(j0 + u) * x[u];
+      for (int u = 0; u < kMergeBatch; ++u)
+        x[u] = (live && j0 + u < n) ? Vec8<TS>::load(st + (int64_t)a.slots[j0 + u] * slot_elems) : f32x8{};
+#pragma unroll
+      for (int u = 0; u < kMergeBatch; ++u)
+        if (j0 + u < n) acc += weight(j0 + u) * x[u];
+    }
   }
   if (live) {
     Vec8<TO>::store((TO*)a.out + row * D + ch * 8, acc);

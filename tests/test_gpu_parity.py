@@ -326,6 +326,39 @@ def test_fp32_states_for_bf16_inputs(D):
     assert max_abs(lse.cpu().numpy(), ml) <= TOL["bf16"]["lse"]
 
 
+def test_repeated_launches_bitwise_identical():
+    """Every launch of the same inputs gives the same bits: a race between
+    the waves of a workgroup on the LDS tile ring (a tile overwritten while
+    another wave still reads it) shows up as launch-to-launch differences.
+    Keys differ strongly from tile to tile so that a stale or early tile
+    changes the result."""
+    import torch
+    a = api()
+    rng = np.random.default_rng(2024)
+    B, H, q_len, D = 1, 16, 1000, 128
+    lens = [700, 333, 64, 901]
+    S = sum(lens)
+    offs = [0]
+    for n in lens:
+        offs.append(offs[-1] + n)
+    P = len(lens)
+    q = rng.standard_normal((B, q_len, H, D), dtype=np.float32) * 4.0
+    k = rng.standard_normal((B, S, H, D), dtype=np.float32)
+    k *= np.repeat(rng.uniform(0.1, 1.5, size=(S + 63) // 64), 64)[:S].astype(np.float32)[None, :, None, None]
+    v = rng.standard_normal((B, S, H, D), dtype=np.float32)
+    qg, kg, vg = (to_gpu(t, "bf16") for t in (q, k, v))
+    first = None
+    for rep in range(8):
+        st, ls = new_state_cache(P, B, q_len, H, D, "bf16")
+        a.attn_partition_states(qg, kg, vg, offs, [1] * P, 1 / math.sqrt(D), st, ls)
+        torch.cuda.synchronize()
+        cur = (st.view(torch.int16).cpu().numpy(), ls.cpu().numpy().view(np.int32))
+        if first is None:
+            first = cur
+        else:
+            assert np.array_equal(cur[0], first[0]) and np.array_equal(cur[1], first[1]), rep
+
+
 def test_unselected_slots_untouched_bitwise():
     import torch
     a = api()
