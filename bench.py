@@ -38,8 +38,8 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # elementwise copy reads / writes 1 GiB), keyed by the build id (source and
 # compile options) of the kernel they were taken on; reported only while the
 # build id matches.
-ATTN_TRAFFIC = {"build_id": "30667f72321ee26d", "workload": "videodit_bf16_h40_d128_s75600_p8",
-                "fetch_bytes": 746950 * 1024 * 2.0, "write_bytes": 287958 * 1024 * 1.0}
+ATTN_TRAFFIC = {"build_id": "73773e472e6228cf", "workload": "videodit_bf16_h40_d128_s75600_p8",
+                "fetch_bytes": 746680 * 1024 * 2.0, "write_bytes": 287957 * 1024 * 1.0}
 
 
 def parse():
