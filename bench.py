@@ -78,6 +78,17 @@ def algorithmic(w, select):
     return flops, merge_bytes, contrib_bytes
 
 
+# MFMA utilisation of the same attention build at the same workload, from
+# rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_LDS_BANK_CONFLICT
+# (busy fraction = busy cycles / (1024 SIMDs x GRBM cycles / 8 XCDs); clock =
+# GRBM cycles / 8 / the traced kernel duration); reported under the same rule.
+ATTN_COUNTERS = {"mfma_busy": 0.605, "lds_bank_conflicts": 0, "clock_ghz": 1.84}
+
+
+def attn_counters(w, select):
+    return dict(ATTN_COUNTERS) if attn_traffic(w, select) is not None else None
+
+
 def attn_traffic(w, select):
     """Profiled HBM bytes per attention launch, or None when the kernel build,
     the workload or the selection differs from the one the counters were
@@ -523,7 +534,7 @@ def main():
                    "fresh_fraction": len(select) / w.P},
         "roofline": {"bound": "mfma", "kernel": "attn_bf16_kernel" if w.dtype == "bf16" else "attn_f32_kernel",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": attn_traffic(w, select)},
+                     "traffic": attn_traffic(w, select), "counters": attn_counters(w, select)},
         "kernels_ms": {"attn_partition_states": {"mean": attn_ms, "median": med(t_attn)},
                        "merge_states": {"mean": merge_ms, "median": med(t_merge)},
                        "contrib": {"mean": mean(t_contrib), "median": med(t_contrib)}},
