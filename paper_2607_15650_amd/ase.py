@@ -61,7 +61,11 @@ class ErrorModelSelectiveAttention:
         self.t_a: Optional[int] = None
         self.w: List[float] = []
         self.alpha: List[float] = []
-        self.snap: Dict[int, torch.Tensor] = {}      # step -> OUT(loc) at that step
+        # snapshots of OUT(loc) at the steps still referenced (t_a and every
+        # group's t_c), kept in slots of one preallocated buffer so that the
+        # drift norms read them in place
+        self.snapbuf = torch.zeros((len(self.groups) + 2, B, self.L, H, D), dtype=dtype, device=device)
+        self.snap: Dict[int, int] = {}               # step -> snapbuf slot
         self.corrections: List[float] = []
         self.eps: Optional[float] = None
         nws = max(api.norms_workspace_bytes(B, H, D, self.L, self.P), api.contrib_workspace_bytes(B, H, self.L, self.P))
@@ -72,6 +76,13 @@ class ErrorModelSelectiveAttention:
         out = torch.empty(len(slots), dtype=torch.float32, device=self.device)
         api.state_norms(states, out, self._ws, slots=list(slots), ref=ref)
         return out.cpu().tolist()
+
+    def _snapshot(self, t: int) -> None:
+        """OUT(loc) of step t into a free snapshot slot."""
+        used = set(self.snap.values())
+        slot = next(i for i in range(self.snapbuf.shape[0]) if i not in used)
+        self.snapbuf[slot].copy_(self.cache[self.q])
+        self.snap[t] = slot
 
     def _attn(self, q, k, v, sel, states, lses):
         api.attn_partition_states(q, k, v, self.offsets, sel, self.scale, states, lses)
@@ -95,7 +106,7 @@ class ErrorModelSelectiveAttention:
         else:
             tcs = sorted(set(self.t_c.values()) | {self.t_a})
             cur = self.cache[self.q]
-            d = dict(zip(tcs, self._norms(torch.stack([self.snap[tc] for tc in tcs]), range(len(tcs)), ref=cur)))
+            d = dict(zip(tcs, self._norms(self.snapbuf, [self.snap[tc] for tc in tcs], ref=cur)))
             n_loc = self.alpha_ref
             drift = d[self.t_a] / n_loc if n_loc > 0 else 0.0
             ase = {grp: sum(self.w[j] * self.alpha[j] for j in range(*grp)) * d[self.t_c[grp]] for grp in self.groups}
@@ -117,9 +128,9 @@ class ErrorModelSelectiveAttention:
                 for grp in compute:
                     self._compose_group(self.cache, self.cache_lse, grp)
                     self.t_c[grp] = t
-                self.snap[t] = self.cache[self.q].clone()
+                self._snapshot(t)
         live = set(self.t_c.values()) | {self.t_a}
-        self.snap = {tc: s for tc, s in self.snap.items() if tc in live}
+        self.snap = {tc: i for tc, i in self.snap.items() if tc in live}
         slots = [grp[0] for grp in self.groups] + [self.q]
         out = torch.empty((self.B, self.L, self.H, self.D), dtype=self.dtype, device=self.device)
         lse = torch.empty((self.B, self.H, self.L), dtype=torch.float32, device=self.device)
@@ -153,4 +164,5 @@ class ErrorModelSelectiveAttention:
         self.alpha = [nj / norms[self.q] if norms[self.q] > 0 else 0.0 for nj in norms]
         self.t_a = t
         self.t_c = {grp: t for grp in self.groups}
-        self.snap = {t: self.cache[self.q].clone()}
+        self.snap = {}
+        self._snapshot(t)

@@ -56,13 +56,14 @@ constexpr int kMergeBatch = 8;    // slots whose loads are in flight together
 // the first batch of slots, then the loads of the row's LSEs; it forms the
 // row's maximum, log-sum-exp and weights itself (no cross-lane exchange, no
 // LDS, no barrier) and OUT = sum_j w_j OUT_j in float32.
-// NS > 0: the slot count is the compile-time constant NS (the common
-// partition counts get their own instantiation, free of run-time loop bounds);
-// NS == 0: any count up to kMaxParts, read from the arguments.
-template <typename TS, typename TO, int D, int NS>
+// NMAX bounds the slot count n (read from the arguments): every loop is
+// unrolled over NMAX with wave-uniform guards, so the weights stay in
+// registers and small counts (group composition: 2 slots; a composed step:
+// a handful) use a small, high-occupancy instantiation.
+template <typename TS, typename TO, int D, int NMAX>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a) {
   constexpr int CPR = D / 8;                      // chunks (lanes) per row
-  const int n = NS > 0 ? NS : a.n;
+  const int n = a.n;
   const int64_t c = (int64_t)blockIdx.x * kMergeThreads + threadIdx.x;
   const bool live = c < a.rows * CPR;
   const int64_t row = live ? c / CPR : 0;
@@ -82,7 +83,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   // every lane of the row loads all the row's LSEs (the row's lanes share
   // the addresses, so each load instruction touches one line per row) and
   // forms the weights itself: no cross-lane exchange
-  constexpr int NL = NS > 0 ? NS : kMaxParts;
+  constexpr int NL = NMAX;
   float lv[NL];
   float mx = -INFINITY;
 #pragma unroll
@@ -128,12 +129,14 @@ hipError_t launch_merge_t(const MergeArgs& a, hipStream_t s) {
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   const dim3 g((unsigned)blocks), t(kMergeThreads);
-  switch (a.n) {
-    case 4: hipLaunchKernelGGL((merge_kernel<TS, TO, D, 4>), g, t, 0, s, a); break;
-    case 8: hipLaunchKernelGGL((merge_kernel<TS, TO, D, 8>), g, t, 0, s, a); break;
-    case 16: hipLaunchKernelGGL((merge_kernel<TS, TO, D, 16>), g, t, 0, s, a); break;
-    default: hipLaunchKernelGGL((merge_kernel<TS, TO, D, 0>), g, t, 0, s, a); break;
-  }
+  if (a.n <= 4)
+    hipLaunchKernelGGL((merge_kernel<TS, TO, D, 4>), g, t, 0, s, a);
+  else if (a.n <= 8)
+    hipLaunchKernelGGL((merge_kernel<TS, TO, D, 8>), g, t, 0, s, a);
+  else if (a.n <= 16)
+    hipLaunchKernelGGL((merge_kernel<TS, TO, D, 16>), g, t, 0, s, a);
+  else
+    hipLaunchKernelGGL((merge_kernel<TS, TO, D, kMaxParts>), g, t, 0, s, a);
   return hipGetLastError();
 }
 
