@@ -34,10 +34,12 @@
 //   (4 consecutive keys x 4 units) hit 16 distinct 16-byte bank groups.
 //
 // Pipeline
-//   Iteration i computes the scores of tile i+1 (MFMA) in the same basic block
-//   as the exponentials of tile i (VALU), then accumulates P_i V_i (MFMA).
-//   The loads of K_{i+2} and V_{i+1} are in flight during the whole
-//   iteration.
+//   D=128 (two waves per SIMD): iteration i computes the scores of tile i+1
+//   (MFMA) in the same basic block as the exponentials of tile i (VALU), then
+//   accumulates P_i V_i (MFMA).  The loads of K_{i+2} and V_{i+1} are in
+//   flight during the whole iteration.  D=64 (three waves per SIMD): tile by
+//   tile, scores, exponentials and P V of tile i while tile i+1 loads; the
+//   other waves of the SIMD overlap the phases.
 //
 // Running maximum
 //   No per-tile row maximum is taken.  Probabilities are computed against the
@@ -155,7 +157,7 @@ __device__ __forceinline__ void store4(__bf16* p, const f32x4& x) {
 }
 __device__ __forceinline__ void store4(float* p, const f32x4& x) { *(f32x4*)p = x; }
 
-template <int D, int QB, int NW, int BN, int NBUF, int WPE, typename TS>
+template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
 __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs a) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];   // 2*NBUF tiles
@@ -372,6 +374,25 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
     for (int qb = 0; qb < QB; ++qb) l[qb] += ls[qb];
   };
 
+  // O^T += V^T P^T over the key steps of a tile; the V operands of key step
+  // s+1 are read while the MFMAs of step s run
+  auto pv = [&](const unsigned char* v_cur, const bf16x8 (&pf)[QB][C::PS]) {
+    bf16x8 va[2][C::DB];
+#pragma unroll
+    for (int db = 0; db < C::DB; ++db) va[0][db] = v_frag(v_cur, 0, db);
+#pragma unroll
+    for (int s = 0; s < C::PS; ++s) {
+      if (s + 1 < C::PS) {
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db) va[(s + 1) & 1][db] = v_frag(v_cur, s + 1, db);
+      }
+#pragma unroll
+      for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma32(va[s & 1][db], pf[qb][s], o[qb][db]);
+    }
+  };
+
   // One pipelined iteration over key tile i.  On entry S_i holds the scores
   // of tile i.  Block A: the MFMAs of S_{i+1} = K_{i+1} Q^T run while the VALU
   // turns S_i into probabilities P_i (exp2, row sums, bf16).  Block B: the
@@ -389,22 +410,7 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
     qk(k_next, snxt);
     bf16x8 pf[QB][C::PS];
     softmax_checked(scur, pf);
-    // O^T += V^T P^T; the V operands of key step s+1 are read while the
-    // MFMAs of step s run
-    bf16x8 va[2][C::DB];
-#pragma unroll
-    for (int db = 0; db < C::DB; ++db) va[0][db] = v_frag(v_cur, 0, db);
-#pragma unroll
-    for (int s = 0; s < C::PS; ++s) {
-      if (s + 1 < C::PS) {
-#pragma unroll
-        for (int db = 0; db < C::DB; ++db) va[(s + 1) & 1][db] = v_frag(v_cur, s + 1, db);
-      }
-#pragma unroll
-      for (int db = 0; db < C::DB; ++db)
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) o[qb][db] = mfma32(va[s & 1][db], pf[qb][s], o[qb][db]);
-    }
+    pv(v_cur, pf);
     // K_{i+2} and V_{i+1}, used by the next iteration, have landed for this
     // wave; the barrier makes that true for the whole workgroup
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));
@@ -412,25 +418,54 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   };
 
   const int n_tiles = (kv_len + BN - 1) / BN;
-  f32x16 s0[C::KB][QB], s1[C::KB][QB];
-  if (n_tiles > 0) {
-    // K_0, then the loads iterations -PF..-1 would have issued, in the same
-    // order as the loop issues them
-    load_tile(kg, kbuf_lds(0), 0, true);
+  if constexpr (SEQ) {
+    // Tile by tile: scores, probabilities, PV.  Used with three waves per
+    // SIMD, where the other waves of the SIMD fill the MFMA and VALU gaps of
+    // each wave's dependent sequence and the smaller register footprint of
+    // this loop is what allows the third wave.
+    if (n_tiles > 0) {
 #pragma unroll
-    for (int j = -C::PF; j < 0; ++j) {
-      load_tile(kg, kbuf_lds(j + 1 + C::PF), (j + 1 + C::PF) * BN, true);
-      load_tile(vg, vbuf_lds(j + C::PF), (j + C::PF) * BN, false);
+      for (int j = 0; j < C::PF; ++j) {
+        load_tile(kg, kbuf_lds(j), j * BN, true);
+        load_tile(vg, vbuf_lds(j), j * BN, false);
+      }
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // tile 0 has landed
+      __syncthreads();
+      for (int i = 0; i < n_tiles; ++i) {
+        // tile i+PF replaces tile i+PF-NBUF, consumed before the last barrier
+        load_tile(kg, kbuf_lds(i + C::PF), (i + C::PF) * BN, true);
+        load_tile(vg, vbuf_lds(i + C::PF), (i + C::PF) * BN, false);
+        f32x16 sc[C::KB][QB];
+        qk(kbuf(i), sc);
+        if ((i + 1) * BN > kv_len) mask_tail(sc, i * BN);
+        bf16x8 pf[QB][C::PS];
+        softmax_checked(sc, pf);
+        pv(vbuf(i), pf);
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // tile i+1 has landed
+        __syncthreads();
+      }
     }
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_0, K_1, V_0 have landed
-    __syncthreads();
-    qk(kbuf(0), s0);
-    // every wave has read K_0 before iteration 0 loads K_2 into its slot
-    __syncthreads();
-    // K_i is consumed one iteration early (scores of the next tile)
-    for (int i = 0; i < n_tiles; i += 2) {
-      iteration(i, s0, s1);
-      if (i + 1 < n_tiles) iteration(i + 1, s1, s0);
+  } else {
+    f32x16 s0[C::KB][QB], s1[C::KB][QB];
+    if (n_tiles > 0) {
+      // K_0, then the loads iterations -PF..-1 would have issued, in the same
+      // order as the loop issues them
+      load_tile(kg, kbuf_lds(0), 0, true);
+#pragma unroll
+      for (int j = -C::PF; j < 0; ++j) {
+        load_tile(kg, kbuf_lds(j + 1 + C::PF), (j + 1 + C::PF) * BN, true);
+        load_tile(vg, vbuf_lds(j + C::PF), (j + C::PF) * BN, false);
+      }
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_0, K_1, V_0 have landed
+      __syncthreads();
+      qk(kbuf(0), s0);
+      // every wave has read K_0 before iteration 0 loads K_2 into its slot
+      __syncthreads();
+      // K_i is consumed one iteration early (scores of the next tile)
+      for (int i = 0; i < n_tiles; i += 2) {
+        iteration(i, s0, s1);
+        if (i + 1 < n_tiles) iteration(i + 1, s1, s0);
+      }
     }
   }
 
@@ -462,12 +497,12 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   }
 }
 
-template <int D, int QB, int NW, int BN, int NBUF, int WPE, typename TS>
+template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
 hipError_t launch_cfg(const AttnArgs& a0, hipStream_t s) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
   const size_t lds = (size_t)2 * NBUF * C::TILEB;
   static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, TS>,
+      (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>,
       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (attr != hipSuccess) return attr;
   AttnArgs a = a0;
@@ -475,21 +510,25 @@ hipError_t launch_cfg(const AttnArgs& a0, hipStream_t s) {
   const int64_t nblk = (int64_t)a.q_tiles * a.H * a.B * a.n_sel;
   if (nblk <= 0) return hipSuccess;
   if (nblk > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, TS>), dim3((unsigned)nblk), dim3(C::NT), lds,
+  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>), dim3((unsigned)nblk), dim3(C::NT), lds,
                      s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-// Tile configuration (query blocks per wave, waves per workgroup, keys per
-// tile, K/V ring size, minimum waves per SIMD) per head dim; overridable at
-// build time for tuning sweeps.
+// Tile configuration per head dim: query blocks per wave, waves per
+// workgroup, keys per tile, K/V ring size, minimum waves per SIMD, and the
+// loop form (pipelined, or tile by tile).  D=128: 8 waves, two per SIMD,
+// pipelined (256 VGPRs).  D=64: 12 waves, three per SIMD, 96-key tiles, tile
+// by tile (166 VGPRs): the softmax VALU work per MFMA doubles at D=64, and a
+// third wave per SIMD hides more of it than software pipelining does.
+// Overridable at build time for tuning sweeps.
 #ifndef DITANGO_D128_CFG
-#define DITANGO_D128_CFG 1, 8, 64, 2, 2
+#define DITANGO_D128_CFG 1, 8, 64, 2, 2, false
 #endif
 #ifndef DITANGO_D64_CFG
-#define DITANGO_D64_CFG 1, 8, 64, 2, 2
+#define DITANGO_D64_CFG 1, 12, 96, 2, 3, true
 #endif
 
 hipError_t launch_attn_bf16(const AttnArgs& a, int D, bool state_f32, hipStream_t s) {
