@@ -38,8 +38,8 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # elementwise copy reads / writes 1 GiB), keyed by the build id (source and
 # compile options) of the kernel they were taken on; reported only while the
 # build id matches.
-ATTN_TRAFFIC = {"build_id": "73773e472e6228cf", "workload": "videodit_bf16_h40_d128_s75600_p8",
-                "fetch_bytes": 746680 * 1024 * 2.0, "write_bytes": 287957 * 1024 * 1.0}
+ATTN_TRAFFIC = {"build_id": "d6bd9cf8c8e3372f", "workload": "videodit_bf16_h40_d128_s75600_p8",
+                "fetch_bytes": 746676 * 1024 * 2.0, "write_bytes": 287956 * 1024 * 1.0}
 
 
 def parse():
@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--eps-local", type=float, default=0.1)
     ap.add_argument("--sweep", action="store_true",
                     help="time the step for each selection of the workload's sweep (long-context workload)")
+    ap.add_argument("--power-seconds", type=float, default=3.0,
+                    help="sample socket power and clocks for this long per kernel after timing (0 disables)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before timing, run one plain elementwise copy of this many MiB "
                          "(the reference kernel that scales profiler byte counters)")
@@ -82,7 +84,7 @@ def algorithmic(w, select):
 # rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_LDS_BANK_CONFLICT
 # (busy fraction = busy cycles / (1024 SIMDs x GRBM cycles / 8 XCDs); clock =
 # GRBM cycles / 8 / the traced kernel duration); reported under the same rule.
-ATTN_COUNTERS = {"mfma_busy": 0.605, "lds_bank_conflicts": 0, "clock_ghz": 1.84}
+ATTN_COUNTERS = {"mfma_busy": 0.596, "lds_bank_conflicts": 0, "clock_ghz": 1.78}
 
 
 def attn_counters(w, select):
@@ -189,6 +191,50 @@ def device_reference(torch):
     return {"bf16_mfma_probe_tflops": probe_flops[0] / (probe_ms * 1e-3) / 1e12,
             "bf16_gemm_8192_tflops": 2 * n ** 3 / (gemm_ms * 1e-3) / 1e12,
             "copy_1gib_gbs": 2 * (1 << 30) / (copy_ms * 1e-3) / 1e9}
+
+
+def power_during(torch, fn, seconds=3.0):
+    """Socket power and XCD (GFX) clocks sampled with amd-smi while fn runs
+    back to back for about `seconds`: shows whether a kernel runs at the
+    power limit (and at what clock).  None when amd-smi is unavailable."""
+    import re
+    import shutil
+    import subprocess
+    import threading
+    tool = shutil.which("amd-smi")
+    if tool is None:
+        return None
+    samples, done = [], threading.Event()
+
+    def sampler():
+        while not done.is_set():
+            try:
+                r = subprocess.run([tool, "metric", "-p", "-c"], capture_output=True, text=True, timeout=10)
+            except Exception:
+                return
+            pw = re.findall(r"SOCKET_POWER:\s*([0-9.]+)\s*W", r.stdout)
+            clk = re.findall(r"GFX_\d+:\s*\n\s*CLK:\s*([0-9.]+)\s*MHz", r.stdout)
+            if pw and clk:
+                samples.append((float(pw[0]), [float(c) for c in clk]))
+            done.wait(0.2)
+
+    fn()
+    torch.cuda.synchronize()
+    th = threading.Thread(target=sampler, daemon=True)
+    th.start()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(4):
+            fn()
+        torch.cuda.synchronize()
+    done.set()
+    th.join(timeout=15)
+    use = samples[1:] or samples      # the first sample can predate the load
+    if not use:
+        return None
+    clocks = [c for _, cs in use for c in cs]
+    return {"socket_w": sum(p for p, _ in use) / len(use), "gfx_mhz_mean": sum(clocks) / len(clocks),
+            "gfx_mhz_min": min(clocks), "gfx_mhz_max": max(clocks), "samples": len(use)}
 
 
 def multistep(args, w):
@@ -507,6 +553,18 @@ def main():
     ref = device_reference(torch)
     if w.dtype == "bf16":
         ref["attn_frac_of_probe"] = achieved / ref["bf16_mfma_probe_tflops"]
+    # power and clocks while the attention kernel, then the MFMA-only probe,
+    # run back to back (after the timed passes, so timing is unaffected)
+    n_wg = 2 * torch.cuda.get_device_properties(0).multi_processor_count
+    sink = torch.empty(n_wg * 256, dtype=torch.float32, device="cuda")
+    if args.power_seconds > 0:
+        ref["power"] = {
+            "attn_partition_states": power_during(
+                torch, lambda: api.attn_partition_states(q, k, v, offs, mask, w.scale, out_states, lse_states),
+                args.power_seconds),
+            "mfma_probe": power_during(torch, lambda: api.probe_mfma_bf16(n_wg, 20000, sink), args.power_seconds),
+        }
+    del sink
 
     cpu = None
     if args.cpu_seconds > 0:
