@@ -190,6 +190,11 @@ EDGE = [
     ("bf16", 64, 2, 1, [7, 64, 129]),
     ("bf16", 128, 1, 257, [256, 255, 1]),
     ("bf16", 64, 5, 513, [100, 0, 333]),
+    # exact multiples of the key tiles (64 at D=128, 96 at D=64) and of the
+    # query tiles (256 rows at D=128, 384 at D=64), and one key either side
+    ("bf16", 128, 2, 256, [64, 128, 63, 65]),
+    ("bf16", 64, 4, 384, [96, 192, 95, 97]),
+    ("bf16", 64, 1, 385, [288, 1, 383]),
     ("f32", 128, 2, 129, [31, 33, 96]),
     ("f32", 64, 3, 40, [0, 5, 70]),
 ]
