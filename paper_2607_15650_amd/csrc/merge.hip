@@ -148,58 +148,102 @@ hipError_t launch_merge_d(const MergeArgs& a, int D, hipStream_t s) {
 }
 
 // ---- contribution weights: per-workgroup partial sums, fixed order
+//
+// Every thread forms the weights of its rows for all listed partitions at
+// once (P accumulators in registers), then each partition's sum is reduced
+// with a butterfly over the wave (lane l adds lane l^k's value, so every lane
+// holds the same bits) and the waves' sums are added in wave order: one
+// barrier for all partitions, and bitwise the same result on every run.
+constexpr int kContribWaves = kContribThreads / 64;
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int k = 32; k > 0; k >>= 1) x += __shfl_xor(x, k, 64);
+  return x;
+}
+
+template <int PMAX>
 __global__ __launch_bounds__(kContribThreads) void contrib_partial_kernel(const ContribArgs a) {
-  __shared__ float red[kContribThreads];
+  __shared__ float red[kContribWaves][PMAX];
   const int tid = threadIdx.x;
+  const int P = a.P;
   const int64_t base = (int64_t)blockIdx.x * kContribRowsPerBlock;
-  float lse_row[kContribRowsPerThread];
+  float acc[PMAX];
+#pragma unroll
+  for (int j = 0; j < PMAX; ++j) acc[j] = 0.f;
 #pragma unroll
   for (int i = 0; i < kContribRowsPerThread; ++i) {
     const int64_t r = base + i * kContribThreads + tid;
-    lse_row[i] = r < a.n_rows ? a.lse_out[r] : -INFINITY;
+    if (r < a.n_rows) {
+      const float lo = a.lse_out[r];
+#pragma unroll
+      for (int j = 0; j < PMAX; ++j) {
+        if (j < P) {
+          const float lj = a.lse[(int64_t)j * a.n_rows + r];
+          float w = 0.f;
+          if (lo != -INFINITY && lj != -INFINITY) w = __builtin_amdgcn_exp2f((lj - lo) * kLog2e);
+          if (a.w_rows != nullptr) a.w_rows[r * P + j] = w;
+          acc[j] += w;
+        }
+      }
+    }
   }
-  for (int j = 0; j < a.P; ++j) {
+#pragma unroll
+  for (int j = 0; j < PMAX; ++j)
+    if (j < P) acc[j] = wave_sum(acc[j]);
+  if ((tid & 63) == 0) {
+#pragma unroll
+    for (int j = 0; j < PMAX; ++j)
+      if (j < P) red[tid >> 6][j] = acc[j];
+  }
+  __syncthreads();
+  if (tid < P) {
     float sum = 0.f;
 #pragma unroll
-    for (int i = 0; i < kContribRowsPerThread; ++i) {
-      const int64_t r = base + i * kContribThreads + tid;
-      float w = 0.f;
-      if (r < a.n_rows) {
-        const float lj = a.lse[(int64_t)j * a.n_rows + r];
-        if (lse_row[i] != -INFINITY && lj != -INFINITY)
-          w = __builtin_amdgcn_exp2f((lj - lse_row[i]) * kLog2e);
-        if (a.w_rows != nullptr) a.w_rows[r * a.P + j] = w;
-      }
-      sum += w;
-    }
-    red[tid] = sum;
-    __syncthreads();
-#pragma unroll
-    for (int off = kContribThreads / 2; off > 0; off >>= 1) {
-      if (tid < off) red[tid] += red[tid + off];
-      __syncthreads();
-    }
-    if (tid == 0) a.partial[(int64_t)blockIdx.x * a.P + j] = red[0];
-    __syncthreads();
+    for (int w = 0; w < kContribWaves; ++w) sum += red[w][tid];
+    a.partial[(int64_t)blockIdx.x * P + tid] = sum;
   }
 }
 
+template <int PMAX>
 __global__ __launch_bounds__(kContribThreads) void contrib_final_kernel(const ContribArgs a) {
-  __shared__ float red[kContribThreads];
+  __shared__ float red[kContribWaves][PMAX];
   const int tid = threadIdx.x;
-  for (int j = 0; j < a.P; ++j) {
-    float sum = 0.f;
-    for (int blk = tid; blk < a.n_blocks; blk += kContribThreads) sum += a.partial[(int64_t)blk * a.P + j];
-    red[tid] = sum;
-    __syncthreads();
+  const int P = a.P;
+  float acc[PMAX];
 #pragma unroll
-    for (int off = kContribThreads / 2; off > 0; off >>= 1) {
-      if (tid < off) red[tid] += red[tid + off];
-      __syncthreads();
-    }
-    if (tid == 0) a.w_part[j] = a.n_rows > 0 ? red[0] / (float)a.n_rows : 0.f;
-    __syncthreads();
+  for (int j = 0; j < PMAX; ++j) acc[j] = 0.f;
+  for (int blk = tid; blk < a.n_blocks; blk += kContribThreads) {
+#pragma unroll
+    for (int j = 0; j < PMAX; ++j)
+      if (j < P) acc[j] += a.partial[(int64_t)blk * P + j];
   }
+#pragma unroll
+  for (int j = 0; j < PMAX; ++j)
+    if (j < P) acc[j] = wave_sum(acc[j]);
+  if ((tid & 63) == 0) {
+#pragma unroll
+    for (int j = 0; j < PMAX; ++j)
+      if (j < P) red[tid >> 6][j] = acc[j];
+  }
+  __syncthreads();
+  if (tid < P) {
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kContribWaves; ++w) sum += red[w][tid];
+    a.w_part[tid] = a.n_rows > 0 ? sum / (float)a.n_rows : 0.f;
+  }
+}
+
+template <int PMAX>
+hipError_t launch_contrib_t(const ContribArgs& a, hipStream_t s) {
+  if (a.n_blocks > 0) {
+    hipLaunchKernelGGL(contrib_partial_kernel<PMAX>, dim3(a.n_blocks), dim3(kContribThreads), 0, s, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(contrib_final_kernel<PMAX>, dim3(1), dim3(kContribThreads), 0, s, a);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -213,13 +257,9 @@ hipError_t launch_merge(const MergeArgs& a, ditango_dtype sdt, ditango_dtype odt
 }
 
 hipError_t launch_contrib(const ContribArgs& a, hipStream_t s) {
-  if (a.n_blocks > 0) {
-    hipLaunchKernelGGL(contrib_partial_kernel, dim3(a.n_blocks), dim3(kContribThreads), 0, s, a);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  hipLaunchKernelGGL(contrib_final_kernel, dim3(1), dim3(kContribThreads), 0, s, a);
-  return hipGetLastError();
+  if (a.P <= 8) return launch_contrib_t<8>(a, s);
+  if (a.P <= 16) return launch_contrib_t<16>(a, s);
+  return launch_contrib_t<kMaxParts>(a, s);
 }
 
 }  // namespace ditango
