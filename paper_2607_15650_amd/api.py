@@ -42,6 +42,9 @@ def _dev(*ts: torch.Tensor) -> None:
             dev = t.device
         elif t.device != dev:
             raise ValueError("all tensors must be on one device")
+    # the kernels are enqueued on the current device's current stream
+    if dev is not None and dev.index != torch.cuda.current_device():
+        raise ValueError("tensors must be on the current device (torch.cuda.set_device)")
 
 
 def _stream() -> int:
