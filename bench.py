@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--eps-local", type=float, default=0.1)
     ap.add_argument("--sweep", action="store_true",
                     help="time the step for each selection of the workload's sweep (long-context workload)")
+    ap.add_argument("--no-selection-sweep", dest="selection_sweep", action="store_false",
+                    help="skip the step-time-against-selected-fraction points")
     ap.add_argument("--power-seconds", type=float, default=3.0,
                     help="sample socket power and clocks for this long per kernel after timing (0 disables)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -85,6 +87,20 @@ def algorithmic(w, select):
 # (busy fraction = busy cycles / (1024 SIMDs x GRBM cycles / 8 XCDs); clock =
 # GRBM cycles / 8 / the traced kernel duration); reported under the same rule.
 ATTN_COUNTERS = {"mfma_busy": 0.596, "lds_bank_conflicts": 0, "clock_ghz": 1.78}
+
+
+# HBM bytes per launch of the merge kernel at the default workload (all P
+# slots), from the same two counter runs and scaled the same way; reported
+# only while merge.hip's build id matches.
+MERGE_TRAFFIC = {"build_id": "86e5c5660225d068", "workload": "videodit_bf16_h40_d128_s75600_p8",
+                 "fetch_bytes": 401743.5 * 1024 * 2.0, "write_bytes": 100409 * 1024 * 1.0}
+
+
+def merge_traffic(w):
+    from paper_2607_15650_amd import build
+    if build.source_id("merge.hip") != MERGE_TRAFFIC["build_id"] or w.name != MERGE_TRAFFIC["workload"]:
+        return None
+    return MERGE_TRAFFIC["fetch_bytes"] + MERGE_TRAFFIC["write_bytes"]
 
 
 def attn_counters(w, select):
@@ -550,6 +566,43 @@ def main():
     del flush
     merge_cold_ms = mean(t_cold)
 
+    # step time against the fraction of partitions computed fresh: the same
+    # step with nearest-first selections of k partitions (the others reused),
+    # and a least-squares line through the points
+    from fixtures.workloads import nearest_first
+    scaling = None
+    if args.selection_sweep and w.P > 1:
+        ks = sorted(set([1, 2, len(select), (w.P + 1) // 2, w.P]))
+        pts = []
+        for kk in ks:
+            sel_k = nearest_first(w.P, w.q, kk)
+            mask_k = [1 if j in sel_k else 0 for j in range(w.P)]
+
+            def step_k():
+                api.attn_partition_states(q, k, v, offs, mask_k, w.scale, out_states, lse_states)
+                api.merge_states(out_states, lse_states, out, lse)
+                api.contrib(lse_states, lse, w_part, ws)
+            step_k()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            n_it = max(3, min(args.steps, 10))
+            e0.record()
+            for _ in range(n_it):
+                step_k()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / n_it
+            pts.append({"k": kk, "fraction": kk / w.P, "fresh": list(sel_k), "ms_per_step": ms,
+                        "tflops": algorithmic(w, sel_k)[0] / (ms * 1e-3) / 1e12})
+        xs = [p_["fraction"] for p_ in pts]
+        ys = [p_["ms_per_step"] for p_ in pts]
+        mx, my = mean(xs), mean(ys)
+        slope = sum((x_ - mx) * (y_ - my) for x_, y_ in zip(xs, ys)) / sum((x_ - mx) ** 2 for x_ in xs)
+        scaling = {"points": pts, "linear_fit_ms": {"per_unit_fraction": slope, "intercept": my - slope * mx},
+                   "note": "nearest-first selections around the query partition, the other partitions' "
+                           "states read from the cache; 10 steps per point"}
+
     ref = device_reference(torch)
     if w.dtype == "bf16":
         ref["attn_frac_of_probe"] = achieved / ref["bf16_mfma_probe_tflops"]
@@ -598,10 +651,12 @@ def main():
                        "contrib": {"mean": mean(t_contrib), "median": med(t_contrib)}},
         "merge_roofline": {"bound": "hbm", "achieved": merge_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                            "frac": merge_gbs / PEAK_HBM_GBS, "bytes_per_launch": merge_bytes,
+                           "traffic": merge_traffic(w),
                            "cold_cache": {"ms": merge_cold_ms,
                                           "achieved": merge_bytes / (merge_cold_ms * 1e-3) / 1e9,
                                           "frac": merge_bytes / (merge_cold_ms * 1e-3) / 1e9 / PEAK_HBM_GBS}},
         "attn_tflops_per_step_flops": flops / 1e12,
+        "selection_scaling": scaling,
         "device_reference": ref,
         "cpu_baseline": cpu,
         "input_gen_s": t_gen,
