@@ -1,0 +1,163 @@
+"""Pins of the multi-step oracles (group states with Dynamic Group State
+Compose, and the error-model planner of Alg. 1) against things other than
+themselves, on the CPU.
+
+What fixes the expected values:
+* composition is exact (Sec. 2.2.4, Eq. composition): with the same tensors
+  at every step, any mix of fresh, reused and composed group states must
+  give full softmax attention, whatever the grouping, budget or selection;
+* the grouping and compose rules of Sec. 4.2.1 and Sec. 5.1 worked by hand
+  on a small case;
+* a construction where the error model's inputs have closed forms: scaling
+  V by (1 + c) scales every partition's OUT by (1 + c) and leaves every LSE
+  (hence every weight) unchanged, so the local drift is exactly c and the
+  extrapolated error of a group (Eq. ase_decomposition with the scale ratios
+  of Eq. scale_ratio and the local drift of Eq. error_extrapolation) is
+  exactly c * sum_{j in G} w_j ||OUT_j||.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from oracle import ase_planner, groups as og
+from fixtures.workloads import partition_offsets
+
+
+def seq(seed, S=40, H=2, D=8, B=1):
+    rng = np.random.default_rng(seed)
+    return {n: rng.standard_normal((B, S, H, D)) for n in ("q", "k", "v")}
+
+
+def full(x, offs, q, scale):
+    return oracle.full_attention(x["q"][:, offs[q]:offs[q + 1]], x["k"], x["v"], scale)
+
+
+# ------------------------------------------------ group states and compose
+
+@pytest.mark.parametrize("g,k,max_states,thr", [(1, 2, 99, 0.1), (2, 2, 2, 0.0), (2, 3, 1, 0.2), (3, 2, 1, 1.0)])
+def test_group_run_with_unchanged_tensors_is_full_attention(g, k, max_states, thr):
+    x = seq(3)
+    S, P, q, scale = 40, 8, 3, 0.35
+    offs = partition_offsets(S, P)
+    res = og.run([x] * 5, offs, q, g, k, max_states, anchors=(0,), threshold=thr, scale=scale)
+    fo, fl = full(x, offs, q, scale)
+    for groups, compute, out, lse, w in res:
+        np.testing.assert_allclose(out, fo, rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(lse, fl, rtol=1e-13)
+        np.testing.assert_allclose(np.sum(w, axis=0), 1.0, rtol=1e-12)
+
+
+def test_group_run_worked_example_of_the_compose_rule():
+    # P=8, local partition 3, g=2: base groups {0,1} {2} {4,5} {6,7}
+    # (Sec. 4.2.1, the local partition kept apart); at a non-anchor step with
+    # room for 2 cached group states, runs of k=2 adjacent groups are composed:
+    # {0,1}+{2} -> {0,1,2}, {4,5}+{6,7} -> {4..7} (Sec. 5.1, Eq. GroupCompose)
+    x = seq(4)
+    offs = partition_offsets(40, 8)
+    res = og.run([x] * 3, offs, 3, 2, 2, 2, anchors=(0,), threshold=1.0, scale=0.35)
+    assert res[0][0] == [(0, 2), (2, 3), (4, 6), (6, 8)]        # anchor: base grouping, all computed
+    assert res[0][1] == [(0, 2), (2, 3), (4, 6), (6, 8)]
+    assert res[1][0] == [(0, 3), (4, 8)]                        # composed under the budget
+    assert res[1][1] == []                                      # threshold 1.0: nothing recomputed
+    assert res[2][0] == [(0, 3), (4, 8)]
+
+
+def test_group_run_reused_states_come_from_their_own_step():
+    # changed tensors: a group that is not recomputed keeps the state of the
+    # step where it was last computed, composed from that step's tensors
+    S, P, q, scale = 40, 8, 3, 0.35
+    offs = partition_offsets(S, P)
+    xs = [seq(10 + s) for s in range(3)]
+    res = og.run(xs, offs, q, 2, 2, 99, anchors=(0,), threshold=1.0, scale=scale)
+    qx = [x["q"][:, offs[q]:offs[q + 1]] for x in xs]
+    # threshold 1.0: after the anchor at step 0 no group is recomputed, so at
+    # step 2 every group state is the one computed at step 0 (from step 0's
+    # queries, keys and values), composed with step 2's local state
+    sts0 = [oracle.partition_state(qx[0], xs[0]["k"][:, offs[j]:offs[j + 1]], xs[0]["v"][:, offs[j]:offs[j + 1]],
+                                   scale) for j in range(P) if j != q]
+    local2 = oracle.partition_state(qx[2], xs[2]["k"][:, offs[q]:offs[q + 1]], xs[2]["v"][:, offs[q]:offs[q + 1]],
+                                    scale)
+    eo, el = oracle.merge([s_[0] for s_ in sts0] + [local2[0]], [s_[1] for s_ in sts0] + [local2[1]])
+    groups, compute, out, lse, _ = res[2]
+    assert compute == []
+    np.testing.assert_allclose(out, eo, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(lse, el, rtol=1e-13)
+
+
+def test_group_run_budget_and_coverage_invariants():
+    S, P, q = 48, 12, 5
+    offs = partition_offsets(S, P)
+    xs = [seq(20 + s, S=S) for s in range(6)]
+    for g in (1, 2, 3):
+        for k in (2, 3):
+            for max_states in (1, 2, 3, 5):
+                res = og.run(xs, offs, q, g, k, max_states, anchors=(0, 3), threshold=0.15, scale=0.3)
+                base = og.groups_of(P, q, g)
+                for s, (groups, compute, _, _, w) in enumerate(res):
+                    covered = sorted(j for a, b in groups for j in range(a, b))
+                    assert covered == [j for j in range(P) if j != q]          # every partition once
+                    assert all(not (a <= q < b) for a, b in groups)            # never across the local one
+                    assert set(compute) <= set(groups)
+                    assert len(w) == len(groups) + 1
+                    if s in (0, 3):
+                        assert groups == base and compute == base
+                    else:
+                        runs = og.compose_runs(groups, k)
+                        # either within the budget, or no two groups left to compose
+                        assert len(groups) <= max_states or all(len(r) == 1 for r in runs)
+
+
+def test_base_groups_hand_examples():
+    assert og.groups_of(8, 3, 2) == [(0, 2), (2, 3), (4, 6), (6, 8)]
+    assert og.groups_of(8, 5, 4) == [(0, 4), (4, 5), (6, 8)]
+    assert og.groups_of(8, 0, 3) == [(1, 3), (3, 6), (6, 8)]
+    assert og.groups_of(4, 2, 1) == [(0, 1), (1, 2), (3, 4)]
+    assert og.compose_runs([(0, 2), (2, 3), (4, 6), (6, 8)], 2) == [[(0, 2), (2, 3)], [(4, 6), (6, 8)]]
+    assert og.compose_runs([(0, 1), (1, 2), (3, 4)], 3) == [[(0, 1), (1, 2)], [(3, 4)]]
+
+
+# ------------------------------------------------------- error-model planner
+
+def test_quantile_hand_examples():
+    assert ase_planner.r_quantile([4.0, 1.0, 3.0, 2.0], 0.5) == 2.0
+    assert ase_planner.r_quantile([4.0, 1.0, 3.0, 2.0], 0.75) == 3.0
+    assert ase_planner.r_quantile([5.0, 1.0, 3.0], 1.0) == 5.0
+    assert ase_planner.r_quantile([5.0, 1.0, 3.0], 0.0) == 1.0
+    assert ase_planner.r_quantile([7.0], 0.4) == 7.0
+
+
+def test_error_planner_with_unchanged_tensors_reuses_everything_exactly():
+    S, P, q, scale = 40, 8, 3, 0.35
+    offs = partition_offsets(S, P)
+    x = seq(5)
+    res = ase_planner.run([x] * 4, offs, q, 2, 0.5, 0.1, scale)
+    fo, fl = full(x, offs, q, scale)
+    assert res[0]["anchor"]
+    for r in res[1:]:
+        assert not r["anchor"] and r["compute"] == [] and r["drift"] == 0.0
+        assert all(v == 0.0 for v in r["ase"].values())
+    for r in res:
+        np.testing.assert_allclose(r["out"], fo, rtol=1e-12, atol=1e-13)
+        np.testing.assert_allclose(r["lse"], fl, rtol=1e-13)
+
+
+@pytest.mark.parametrize("c", [0.02, 0.3])
+def test_error_planner_closed_forms_under_a_value_scaling(c):
+    S, P, q, scale, g = 40, 8, 3, 0.35, 2
+    offs = partition_offsets(S, P)
+    x0 = seq(6)
+    x1 = dict(x0, v=x0["v"] * (1.0 + c))
+    eps_local = 0.1
+    res = ase_planner.run([x0, x1], offs, q, g, 0.5, eps_local, scale)
+    qx = x0["q"][:, offs[q]:offs[q + 1]]
+    sts = [oracle.partition_state(qx, x0["k"][:, offs[j]:offs[j + 1]], x0["v"][:, offs[j]:offs[j + 1]], scale)
+           for j in range(P)]
+    _, lse = oracle.merge([s_[0] for s_ in sts], [s_[1] for s_ in sts])
+    _, wbar = oracle.contrib([s_[1] for s_ in sts], lse)
+    r = res[1]
+    assert r["drift"] == pytest.approx(c, rel=1e-12)                 # ||dOUT_loc|| / ||OUT_loc||
+    for (a, b), ase in r["ase"].items():
+        expect = c * sum(wbar[j] * np.linalg.norm(sts[j][0]) for j in range(a, b))
+        assert ase == pytest.approx(expect, rel=1e-10)
+    # a relative local drift above eps_local makes the step an anchor (Sec. 4.2.4)
+    assert r["anchor"] == (c > eps_local)
