@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--eps-local", type=float, default=0.1)
     ap.add_argument("--sweep", action="store_true",
                     help="time the step for each selection of the workload's sweep (long-context workload)")
+    ap.add_argument("--no-tail-split", dest="tail_split", action="store_false",
+                    help="launch the attention kernel without the workspace that splits its last round")
     ap.add_argument("--no-selection-sweep", dest="selection_sweep", action="store_false",
                     help="skip the step-time-against-selected-fraction points")
     ap.add_argument("--power-seconds", type=float, default=3.0,
@@ -490,6 +492,12 @@ def main():
     lse = torch.empty((w.B, w.H, q_len), dtype=torch.float32, device="cuda")
     w_part = torch.empty(w.P, dtype=torch.float32, device="cuda")
     ws = torch.empty(max(16, api.contrib_workspace_bytes(w.B, w.H, q_len, w.P)), dtype=torch.uint8, device="cuda")
+    # workspace of the attention launch: lets it split the tasks of a partly
+    # filled last round over key ranges (None when no split helps)
+    def attn_ws(sel_mask):
+        n = api.attn_workspace_bytes(dt, w.B, w.H, w.D, q_len, offs, sel_mask) if args.tail_split else 0
+        return torch.empty(n, dtype=torch.uint8, device="cuda") if n > 0 else None
+    ws_attn = attn_ws(mask)
 
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib * (1 << 20) // 4
@@ -506,7 +514,7 @@ def main():
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        api.attn_partition_states(q, k, v, offs, mask, w.scale, out_states, lse_states)
+        api.attn_partition_states(q, k, v, offs, mask, w.scale, out_states, lse_states, ws_attn)
         if ev is not None:
             ev[1].record()
         api.merge_states(out_states, lse_states, out, lse)
@@ -577,9 +585,10 @@ def main():
         for kk in ks:
             sel_k = nearest_first(w.P, w.q, kk)
             mask_k = [1 if j in sel_k else 0 for j in range(w.P)]
+            ws_k = attn_ws(mask_k)
 
             def step_k():
-                api.attn_partition_states(q, k, v, offs, mask_k, w.scale, out_states, lse_states)
+                api.attn_partition_states(q, k, v, offs, mask_k, w.scale, out_states, lse_states, ws_k)
                 api.merge_states(out_states, lse_states, out, lse)
                 api.contrib(lse_states, lse, w_part, ws)
             step_k()
@@ -613,7 +622,8 @@ def main():
     if args.power_seconds > 0:
         ref["power"] = {
             "attn_partition_states": power_during(
-                torch, lambda: api.attn_partition_states(q, k, v, offs, mask, w.scale, out_states, lse_states),
+                torch, lambda: api.attn_partition_states(q, k, v, offs, mask, w.scale, out_states, lse_states,
+                                                         ws_attn),
                 args.power_seconds),
             "mfma_probe": power_during(torch, lambda: api.probe_mfma_bf16(n_wg, 20000, sink), args.power_seconds),
         }
@@ -642,7 +652,8 @@ def main():
         "data": "synthetic (seeded N(0,1) plus shared sinusoidal positional component)",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "D": w.D, "S": w.S, "P": w.P,
                    "query_partition": w.q, "q_len": q_len, "fresh_partitions": list(select),
-                   "fresh_fraction": len(select) / w.P},
+                   "fresh_fraction": len(select) / w.P,
+                   "attn_workspace_bytes": int(ws_attn.numel()) if ws_attn is not None else 0},
         "roofline": {"bound": "mfma", "kernel": "attn_bf16_kernel" if w.dtype == "bf16" else "attn_f32_kernel",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": attn_traffic(w, select), "counters": attn_counters(w, select)},

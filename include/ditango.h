@@ -103,6 +103,45 @@ ditango_status ditango_attn_partition_states_ex(
     void* out_states, ditango_dtype state_dt, float* lse_states, void* stream);
 
 /*
+ * The same with a workspace that lets the launch balance its last round
+ * (the same computation, Sec. 2.2.4, Eq. attention_state; the partial states
+ * are composed by Eq. composition).  A launch is a set of equal-length tasks
+ * (query tile x head x batch x selected partition) of which the GPU runs a
+ * fixed number at a time; the tasks of a last, partly filled round are each
+ * split into up to 8 key ranges whose partial states go to the workspace and
+ * are composed into their slots by a second, small kernel on `stream`.
+ *
+ *   workspace        device, 256-byte aligned, at least
+ *                    ditango_attn_workspace_bytes(...) bytes for this shape and
+ *                    selection on the current device; NULL or fewer bytes:
+ *                    the launch runs unsplit (the result of
+ *                    ditango_attn_partition_states_ex).  Contents on entry
+ *                    are ignored; on return they are scratch.  Calls that
+ *                    overlap on one workspace race.
+ *   workspace_bytes  its size.
+ *
+ * Split results differ from unsplit ones only by the rounding of the
+ * composition; both are deterministic.  fp32 inputs never split.
+ * DITANGO_ERR_INVALID for a misaligned workspace; otherwise as
+ * ditango_attn_partition_states_ex.
+ */
+ditango_status ditango_attn_partition_states_ws(
+    const void* q, const void* k, const void* v, ditango_dtype dt,
+    int B, int H, int D, int64_t q_len,
+    const int64_t* kv_offsets, int P, const uint8_t* select, float scale,
+    void* out_states, ditango_dtype state_dt, float* lse_states,
+    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Workspace bytes ditango_attn_partition_states_ws needs to split the last
+ * round of this launch on the current HIP device (its compute-unit count and
+ * the kernel's occupancy decide); 0 when no split shortens it, for fp32
+ * inputs, or for invalid arguments.  Host only, enqueues nothing.
+ */
+size_t ditango_attn_workspace_bytes(ditango_dtype dt, int B, int H, int D, int64_t q_len,
+                                    const int64_t* kv_offsets, int P, const uint8_t* select);
+
+/*
  * Composition of cached and fresh states (Sec. 2.2.4, Eq. composition, n-ary):
  *     M = max_j LSE_j,  LSE = M + log sum_j exp(LSE_j - M),
  *     OUT = sum_j exp(LSE_j - LSE) * OUT_j

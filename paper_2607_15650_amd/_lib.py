@@ -30,6 +30,14 @@ SIGNATURES = {
         _c.c_int, _c.c_int, _c.c_int, _c.c_int64,
         _c.POINTER(_c.c_int64), _c.c_int, _c.POINTER(_c.c_uint8), _c.c_float,
         _c.c_void_p, _c.c_int, _c.c_void_p, _c.c_void_p]),
+    "ditango_attn_partition_states_ws": (_c.c_int, [
+        _c.c_void_p, _c.c_void_p, _c.c_void_p, _c.c_int,
+        _c.c_int, _c.c_int, _c.c_int, _c.c_int64,
+        _c.POINTER(_c.c_int64), _c.c_int, _c.POINTER(_c.c_uint8), _c.c_float,
+        _c.c_void_p, _c.c_int, _c.c_void_p, _c.c_void_p, _c.c_size_t, _c.c_void_p]),
+    "ditango_attn_workspace_bytes": (_c.c_size_t, [
+        _c.c_int, _c.c_int, _c.c_int, _c.c_int, _c.c_int64,
+        _c.POINTER(_c.c_int64), _c.c_int, _c.POINTER(_c.c_uint8)]),
     "ditango_merge_states": (_c.c_int, [
         _c.c_void_p, _c.c_void_p, _c.c_int,
         _c.c_int, _c.POINTER(_c.c_int32), _c.c_int,

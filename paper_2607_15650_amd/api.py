@@ -51,14 +51,28 @@ def _stream() -> int:
     return torch.cuda.current_stream().cuda_stream
 
 
+def attn_workspace_bytes(dtype: torch.dtype, B: int, H: int, D: int, q_len: int,
+                         offsets: Sequence[int], select: Sequence[int]) -> int:
+    """Workspace bytes that let attn_partition_states split its last round
+    on the current device (ditango_attn_workspace_bytes); 0 = no split helps."""
+    P = len(offsets) - 1
+    offs = (ctypes.c_int64 * (P + 1))(*[int(x) for x in offsets])
+    sel = (ctypes.c_uint8 * P)(*[1 if s else 0 for s in select])
+    return int(_lib.lib().ditango_attn_workspace_bytes(_DT[dtype], B, H, D, q_len, offs, P, sel))
+
+
 def attn_partition_states(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
                           offsets: Sequence[int], select: Sequence[int], scale: float,
-                          out_states: torch.Tensor, lse_states: torch.Tensor) -> None:
+                          out_states: torch.Tensor, lse_states: torch.Tensor,
+                          workspace: Optional[torch.Tensor] = None) -> None:
     """Fresh states of the selected partitions into their slots
     (ditango_attn_partition_states).  Unselected slots are left untouched.
     ``out_states`` is in the input dtype, or float32 for bf16 inputs
-    (ditango_attn_partition_states_ex: states at full precision)."""
-    _dev(q, k, v, out_states, lse_states)
+    (ditango_attn_partition_states_ex: states at full precision).  With a
+    ``workspace`` (uint8, attn_workspace_bytes(...) bytes, 256-byte aligned)
+    the last round of the launch is split over key ranges
+    (ditango_attn_partition_states_ws)."""
+    _dev(q, k, v, out_states, lse_states, workspace)
     B, q_len, H, D = q.shape
     P = len(offsets) - 1
     if len(select) != P:
@@ -77,7 +91,13 @@ def attn_partition_states(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
         raise ValueError("q, k, v must share a dtype")
     offs = (ctypes.c_int64 * (P + 1))(*[int(x) for x in offsets])
     sel = (ctypes.c_uint8 * P)(*[1 if s else 0 for s in select])
-    if out_states.dtype == q.dtype:
+    if workspace is not None:
+        st = _lib.lib().ditango_attn_partition_states_ws(
+            q.data_ptr(), k.data_ptr(), v.data_ptr(), _dtype(q), B, H, D, q_len,
+            offs, P, sel, float(scale), out_states.data_ptr(), _dtype(out_states), lse_states.data_ptr(),
+            workspace.data_ptr(), workspace.numel() * workspace.element_size(), _stream())
+        _lib.check("ditango_attn_partition_states_ws", st)
+    elif out_states.dtype == q.dtype:
         st = _lib.lib().ditango_attn_partition_states(
             q.data_ptr(), k.data_ptr(), v.data_ptr(), _dtype(q), B, H, D, q_len,
             offs, P, sel, float(scale), out_states.data_ptr(), lse_states.data_ptr(), _stream())

@@ -162,8 +162,16 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   using C = Cfg<D, QB, NW, BN, NBUF>;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];   // 2*NBUF tiles
 
-  // ---- task decode: (selected partition, batch, head, query tile)
-  const int task = xcd_remap(blockIdx.x, gridDim.x);
+  // ---- task decode: (selected partition, batch, head, query tile), and for
+  // a task of the split tail, which of its split_f key ranges
+  int task, part = -1;
+  if ((int)blockIdx.x < a.n_main) {
+    task = xcd_remap(blockIdx.x, a.n_main);
+  } else {
+    const int u = (int)blockIdx.x - a.n_main;
+    task = a.n_main + u / a.split_f;
+    part = u % a.split_f;
+  }
   const int qt = task % a.q_tiles;
   int t = task / a.q_tiles;
   const int h = t % a.H;
@@ -178,9 +186,17 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   const int g = lane >> 5;
 
   const int64_t HD = (int64_t)a.H * D;
-  const int kv_len = a.kv_len[sel];
-  const int64_t kv0 = a.kv_begin[sel];
+  int kv_len = a.kv_len[sel];
+  int64_t kv0 = a.kv_begin[sel];
   const int slot = a.slot[sel];
+  if (part >= 0) {
+    // key range `part` of split_f: whole tiles, the last range the remainder
+    const int per = ((kv_len + BN - 1) / BN + a.split_f - 1) / a.split_f * BN;
+    const int k0 = min(part * per, kv_len);
+    const int k1 = min(k0 + per, kv_len);
+    kv0 += k0;
+    kv_len = k1 - k0;
+  }
 
   const __bf16* __restrict__ qg = (const __bf16*)a.q;
   const __bf16* __restrict__ kg = (const __bf16*)a.k + ((int64_t)b * a.S + kv0) * HD + (int64_t)h * D;
@@ -469,48 +485,182 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
     }
   }
 
-  // ---- epilogue: normalise, write OUT_j and LSE_j of slot j
+  // ---- epilogue: normalise, write OUT_j and LSE_j of slot j (a split
+  // task's range: its partial state, in float32, to the workspace)
   TS* outg = (TS*)a.out_states;
   const int64_t slot_elems = (int64_t)a.B * a.q_len * HD;
+  const int64_t pt = part >= 0 ? (int64_t)(task - a.n_main) * a.split_f + part : 0;
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const float lt = pair_sum(l[qb]);
     const int64_t row = row0 + qb * 32 + lr;
     if (row < a.q_len) {
       const float inv = lt > 0.f ? 1.0f / lt : 0.f;
-      TS* dst = outg + (int64_t)slot * slot_elems + ((int64_t)b * a.q_len + row) * HD +
-                    (int64_t)h * D + 4 * g;
+      const float lse = lt > 0.f ? (m[qb] + __builtin_amdgcn_logf(lt)) * kLn2 : -INFINITY;
+      if (part < 0) {
+        TS* dst = outg + (int64_t)slot * slot_elems + ((int64_t)b * a.q_len + row) * HD +
+                      (int64_t)h * D + 4 * g;
 #pragma unroll
-      for (int db = 0; db < C::DB; ++db)
+        for (int db = 0; db < C::DB; ++db)
 #pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          f32x4 x;
+          for (int r4 = 0; r4 < 4; ++r4) {
+            f32x4 x;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
-          store4(dst + db * 32 + 8 * r4, x);
-        }
-      if (g == 0) {
-        const float lse = lt > 0.f ? (m[qb] + __builtin_amdgcn_logf(lt)) * kLn2 : -INFINITY;
-        a.lse_states[(((int64_t)slot * a.B + b) * a.H + h) * a.q_len + row] = lse;
+            for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
+            store4(dst + db * 32 + 8 * r4, x);
+          }
+        if (g == 0) a.lse_states[(((int64_t)slot * a.B + b) * a.H + h) * a.q_len + row] = lse;
+      } else {
+        const int64_t rl = row - (int64_t)qt * C::BM;            // row within the query tile
+        float* dst = a.part_out + (pt * C::BM + rl) * D + 4 * g;
+#pragma unroll
+        for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) {
+            f32x4 x;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
+            store4(dst + db * 32 + 8 * r4, x);
+          }
+        if (g == 0) a.part_lse[pt * C::BM + rl] = lse;
       }
     }
   }
 }
 
+// Composes the split_f partial states of every split task (Eq. composition
+// over its key ranges) into the task's rows of its slot.  One thread per 8
+// elements of a row.
+template <int D, int BM, typename TS>
+__global__ __launch_bounds__(256) void attn_split_fixup_kernel(const AttnArgs a) {
+  constexpr int CPR = D / 8;
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= (int64_t)a.n_split * BM * CPR) return;
+  const int ch = (int)(c % CPR);
+  const int64_t rr = c / CPR;
+  const int rl = (int)(rr % BM);
+  const int t = (int)(rr / BM);
+  int task = a.n_main + t;
+  const int qt = task % a.q_tiles;
+  task /= a.q_tiles;
+  const int h = task % a.H;
+  task /= a.H;
+  const int b = task % a.B;
+  const int sel = task / a.B;
+  const int64_t row = (int64_t)qt * BM + rl;
+  if (row >= a.q_len) return;
+  const int f = a.split_f;
+  const int64_t p0 = (int64_t)t * f;
+  float lv[kMaxSplit];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int p = 0; p < kMaxSplit; ++p) {
+    lv[p] = p < f ? a.part_lse[(p0 + p) * BM + rl] : -INFINITY;
+    mx = fmaxf(mx, lv[p]);
+  }
+  float tot = 0.f;
+#pragma unroll
+  for (int p = 0; p < kMaxSplit; ++p) {
+    lv[p] = mx == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((lv[p] - mx) * 1.4426950408889634f);
+    tot += lv[p];
+  }
+  const float inv = tot > 0.f ? 1.0f / tot : 0.f;
+  f32x4 acc0 = f32x4{}, acc1 = f32x4{};
+#pragma unroll
+  for (int p = 0; p < kMaxSplit; ++p) {
+    if (p < f) {
+      const float* src = a.part_out + ((p0 + p) * BM + rl) * D + ch * 8;
+      const float w = lv[p] * inv;
+      acc0 += w * *(const f32x4*)src;
+      acc1 += w * *(const f32x4*)(src + 4);
+    }
+  }
+  const int slot = a.slot[sel];
+  const int64_t HD = (int64_t)a.H * D;
+  TS* dst = (TS*)a.out_states + (int64_t)slot * a.B * a.q_len * HD + ((int64_t)b * a.q_len + row) * HD +
+            (int64_t)h * D + ch * 8;
+  store4(dst, acc0);
+  store4(dst + 4, acc1);
+  if (ch == 0)
+    a.lse_states[(((int64_t)slot * a.B + b) * a.H + h) * a.q_len + row] =
+        tot > 0.f ? mx + __builtin_amdgcn_logf(tot) * kLn2 : -INFINITY;
+}
+
+constexpr size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Tail split plan of one launch: the split factor, the number of split
+// tasks and the workspace bytes (partial OUT in float32, then partial LSE).
 template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
-hipError_t launch_cfg(const AttnArgs& a0, hipStream_t s) {
+hipError_t plan_cfg(const AttnArgs& a, int* f_out, int64_t* n_split_out, size_t* bytes_out) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
   const size_t lds = (size_t)2 * NBUF * C::TILEB;
   static const hipError_t attr = hipFuncSetAttribute(
       (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>,
       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (attr != hipSuccess) return attr;
+  *f_out = 1;
+  *n_split_out = 0;
+  *bytes_out = 0;
+  const int64_t nblk = (a.q_len + C::BM - 1) / C::BM * a.H * a.B * a.n_sel;
+  if (nblk <= 0) return hipSuccess;
+  int dev = 0, cus = 0, occ = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &occ, (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>, C::NT, lds);
+  if (e != hipSuccess) return e;
+  const int64_t slots = (int64_t)cus * (occ > 0 ? occ : 1);
+  const int f = plan_tail_split(nblk, slots);
+  if (f <= 1) return hipSuccess;
+  const int64_t n_split = nblk % slots;
+  *f_out = f;
+  *n_split_out = n_split;
+  *bytes_out = align256((size_t)n_split * f * C::BM * D * sizeof(float)) +
+               align256((size_t)n_split * f * C::BM * sizeof(float));
+  return hipSuccess;
+}
+
+template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
+hipError_t launch_cfg(const AttnArgs& a0, void* ws, size_t ws_bytes, hipStream_t s) {
+  using C = Cfg<D, QB, NW, BN, NBUF>;
+  const size_t lds = (size_t)2 * NBUF * C::TILEB;
+  int f = 1;
+  int64_t n_split = 0;
+  size_t need = 0;
+  if (ws != nullptr) {
+    const hipError_t e = plan_cfg<D, QB, NW, BN, NBUF, WPE, SEQ, TS>(a0, &f, &n_split, &need);
+    if (e != hipSuccess) return e;
+  } else {
+    static const hipError_t attr = hipFuncSetAttribute(
+        (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>,
+        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (attr != hipSuccess) return attr;
+  }
   AttnArgs a = a0;
   a.q_tiles = (int)((a.q_len + C::BM - 1) / C::BM);
   const int64_t nblk = (int64_t)a.q_tiles * a.H * a.B * a.n_sel;
   if (nblk <= 0) return hipSuccess;
-  if (nblk > 0x7fffffff) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>), dim3((unsigned)nblk), dim3(C::NT), lds,
+  if (nblk + (int64_t)kMaxSplit * n_split > 0x7fffffff) return hipErrorInvalidConfiguration;
+  int64_t grid = nblk;
+  if (f > 1 && n_split > 0 && ws_bytes >= need) {
+    a.n_main = (int)(nblk - n_split);
+    a.n_split = (int)n_split;
+    a.split_f = f;
+    a.part_out = (float*)ws;
+    a.part_lse = (float*)((char*)ws + align256((size_t)n_split * f * C::BM * D * sizeof(float)));
+    grid = a.n_main + n_split * f;
+  } else {
+    a.n_main = (int)nblk;
+    a.n_split = 0;
+    a.split_f = 1;
+  }
+  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>), dim3((unsigned)grid), dim3(C::NT), lds,
+                     s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.n_split == 0) return e;
+  const int64_t chunks = (int64_t)a.n_split * C::BM * (D / 8);
+  hipLaunchKernelGGL((attn_split_fixup_kernel<D, C::BM, TS>), dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0,
                      s, a);
   return hipGetLastError();
 }
@@ -531,11 +681,29 @@ hipError_t launch_cfg(const AttnArgs& a0, hipStream_t s) {
 #define DITANGO_D64_CFG 1, 12, 96, 2, 3, true
 #endif
 
-hipError_t launch_attn_bf16(const AttnArgs& a, int D, bool state_f32, hipStream_t s) {
+hipError_t launch_attn_bf16_ws(const AttnArgs& a, int D, bool state_f32, void* ws, size_t ws_bytes,
+                               hipStream_t s) {
   if (D == 128)
-    return state_f32 ? launch_cfg<128, DITANGO_D128_CFG, float>(a, s) : launch_cfg<128, DITANGO_D128_CFG, __bf16>(a, s);
+    return state_f32 ? launch_cfg<128, DITANGO_D128_CFG, float>(a, ws, ws_bytes, s)
+                     : launch_cfg<128, DITANGO_D128_CFG, __bf16>(a, ws, ws_bytes, s);
   if (D == 64)
-    return state_f32 ? launch_cfg<64, DITANGO_D64_CFG, float>(a, s) : launch_cfg<64, DITANGO_D64_CFG, __bf16>(a, s);
+    return state_f32 ? launch_cfg<64, DITANGO_D64_CFG, float>(a, ws, ws_bytes, s)
+                     : launch_cfg<64, DITANGO_D64_CFG, __bf16>(a, ws, ws_bytes, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_attn_bf16(const AttnArgs& a, int D, bool state_f32, hipStream_t s) {
+  return launch_attn_bf16_ws(a, D, state_f32, nullptr, 0, s);
+}
+
+hipError_t attn_bf16_split_bytes(const AttnArgs& a, int D, size_t* bytes) {
+  int f = 1;
+  int64_t n_split = 0;
+  *bytes = 0;
+  // the plan depends on the kernel's occupancy, which the state type does
+  // not change; the bf16-state instantiation is queried
+  if (D == 128) return plan_cfg<128, DITANGO_D128_CFG, __bf16>(a, &f, &n_split, bytes);
+  if (D == 64) return plan_cfg<64, DITANGO_D64_CFG, __bf16>(a, &f, &n_split, bytes);
   return hipErrorInvalidValue;
 }
 

@@ -30,11 +30,15 @@ const char* ditango_status_string(ditango_status s) {
 
 const char* ditango_version(void) { return "0.1.0"; }
 
-ditango_status ditango_attn_partition_states_ex(
-    const void* q, const void* k, const void* v, ditango_dtype dt,
-    int B, int H, int D, int64_t q_len,
-    const int64_t* kv_offsets, int P, const uint8_t* select, float scale,
-    void* out_states, ditango_dtype state_dt, float* lse_states, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks shared by the attention entry points; fills `a` (not the
+// launch fields).  Returns DITANGO_OK when a launch may proceed.
+ditango_status attn_args(const void* q, const void* k, const void* v, ditango_dtype dt, int B, int H, int D,
+                         int64_t q_len, const int64_t* kv_offsets, int P, const uint8_t* select, float scale,
+                         const void* out_states, ditango_dtype state_dt, const float* lse_states, AttnArgs* a) {
   if (!q || !k || !v || !kv_offsets || !select || !out_states || !lse_states) return DITANGO_ERR_INVALID;
   if (!valid_dtype(dt) || !valid_dtype(state_dt)) return DITANGO_ERR_INVALID;
   if (state_dt != dt && !(dt == DITANGO_BF16 && state_dt == DITANGO_F32)) return DITANGO_ERR_UNSUPPORTED;
@@ -51,34 +55,77 @@ ditango_status ditango_attn_partition_states_ex(
   // per-partition key count must fit int32 (checked above), so must q_len.
   if (q_len > 0x7fffffffLL) return DITANGO_ERR_UNSUPPORTED;
   // the bf16 kernel addresses a key tile with 32-bit lane offsets from its
-  // first row: H*D <= 65536 keeps a 128-key tile within 16 MiB
+  // first row: H*D <= 65536 keeps a tile of up to 128 keys within 16 MiB
   if ((int64_t)H * D > 65536) return DITANGO_ERR_UNSUPPORTED;
 
-  AttnArgs a;
-  memset(&a, 0, sizeof(a));
-  a.q = q;
-  a.k = k;
-  a.v = v;
-  a.out_states = out_states;
-  a.lse_states = lse_states;
-  a.q_len = q_len;
-  a.S = kv_offsets[P];
-  a.B = B;
-  a.H = H;
-  a.scale_log2 = scale * 1.4426950408889634f;
+  memset(a, 0, sizeof(*a));
+  a->q = q;
+  a->k = k;
+  a->v = v;
+  a->out_states = const_cast<void*>(out_states);
+  a->lse_states = const_cast<float*>(lse_states);
+  a->q_len = q_len;
+  a->S = kv_offsets[P];
+  a->B = B;
+  a->H = H;
+  a->scale_log2 = scale * 1.4426950408889634f;
   int n = 0;
   for (int j = 0; j < P; ++j) {
     if (!select[j]) continue;
-    a.kv_begin[n] = kv_offsets[j];
-    a.kv_len[n] = (int32_t)(kv_offsets[j + 1] - kv_offsets[j]);
-    a.slot[n] = j;
+    a->kv_begin[n] = kv_offsets[j];
+    a->kv_len[n] = (int32_t)(kv_offsets[j + 1] - kv_offsets[j]);
+    a->slot[n] = j;
     ++n;
   }
-  a.n_sel = n;
-  if (n == 0) return DITANGO_OK;
+  a->n_sel = n;
+  return DITANGO_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ditango_status ditango_attn_partition_states_ws(
+    const void* q, const void* k, const void* v, ditango_dtype dt,
+    int B, int H, int D, int64_t q_len,
+    const int64_t* kv_offsets, int P, const uint8_t* select, float scale,
+    void* out_states, ditango_dtype state_dt, float* lse_states,
+    void* workspace, size_t workspace_bytes, void* stream) {
+  AttnArgs a;
+  const ditango_status st = attn_args(q, k, v, dt, B, H, D, q_len, kv_offsets, P, select, scale, out_states,
+                                      state_dt, lse_states, &a);
+  if (st != DITANGO_OK) return st;
+  if (workspace != nullptr && ((uintptr_t)workspace & 255u) != 0) return DITANGO_ERR_INVALID;
+  if (a.n_sel == 0) return DITANGO_OK;
   hipStream_t s = (hipStream_t)stream;
-  if (dt == DITANGO_BF16) return from_hip(launch_attn_bf16(a, D, state_dt == DITANGO_F32, s));
+  if (dt == DITANGO_BF16)
+    return from_hip(launch_attn_bf16_ws(a, D, state_dt == DITANGO_F32, workspace_bytes > 0 ? workspace : nullptr,
+                                        workspace_bytes, s));
   return from_hip(launch_attn_f32(a, D, s));
+}
+
+ditango_status ditango_attn_partition_states_ex(
+    const void* q, const void* k, const void* v, ditango_dtype dt,
+    int B, int H, int D, int64_t q_len,
+    const int64_t* kv_offsets, int P, const uint8_t* select, float scale,
+    void* out_states, ditango_dtype state_dt, float* lse_states, void* stream) {
+  return ditango_attn_partition_states_ws(q, k, v, dt, B, H, D, q_len, kv_offsets, P, select, scale, out_states,
+                                          state_dt, lse_states, nullptr, 0, stream);
+}
+
+size_t ditango_attn_workspace_bytes(ditango_dtype dt, int B, int H, int D, int64_t q_len,
+                                    const int64_t* kv_offsets, int P, const uint8_t* select) {
+  if (dt != DITANGO_BF16) return 0;
+  // placeholders stand in for the tensors: only the shape and the selection
+  // decide the plan
+  static const char dummy[4] = {0};
+  AttnArgs a;
+  if (attn_args(dummy, dummy, dummy, dt, B, H, D, q_len, kv_offsets, P, select, 1.0f, dummy, dt,
+                (const float*)dummy, &a) != DITANGO_OK || a.n_sel == 0)
+    return 0;
+  size_t bytes = 0;
+  if (attn_bf16_split_bytes(a, D, &bytes) != hipSuccess) return 0;
+  return bytes;
 }
 
 ditango_status ditango_attn_partition_states(

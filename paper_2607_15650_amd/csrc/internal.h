@@ -27,7 +27,40 @@ struct AttnArgs {
   int64_t kv_begin[kMaxParts];
   int32_t kv_len[kMaxParts];
   int32_t slot[kMaxParts];
+  // Tail split (bf16 kernel): logical tasks [n_main, n_main + n_split) run
+  // as split_f workgroups each, over consecutive key ranges, writing partial
+  // states to part_out / part_lse; a fix-up kernel composes them into the
+  // slots.  n_split = 0: every task is one workgroup (n_main is set by the
+  // launcher).
+  int n_main;
+  int n_split;
+  int split_f;
+  float* part_out;          // [n_split * split_f][rows per workgroup][D]
+  float* part_lse;          // [n_split * split_f][rows per workgroup]
 };
+
+constexpr int kMaxSplit = 8;
+
+// Tail split plan: with `slots` workgroups resident at once and `tasks`
+// equal-length tasks, the last round runs tasks % slots of them; splitting
+// each of those into f key ranges shortens it to ceil(f * rem / slots) / f
+// of a task.  Returns the f in [2, kMaxSplit] that minimises that (the
+// smallest on ties), or 1 when no split shortens the last round.
+inline int plan_tail_split(int64_t tasks, int64_t slots) {
+  if (slots <= 0) return 1;
+  const int64_t rem = tasks % slots;
+  if (rem == 0) return 1;
+  int best = 1;
+  double best_t = 1.0;
+  for (int f = 2; f <= kMaxSplit; ++f) {
+    const double t = (double)((f * rem + slots - 1) / slots) / f;
+    if (t < best_t - 1e-12) {
+      best_t = t;
+      best = f;
+    }
+  }
+  return best;
+}
 
 struct MergeArgs {
   const void* states;       // [P][rows][D]  (rows = B*q_len*H)
@@ -73,6 +106,13 @@ constexpr int kContribRowsPerBlock = kContribThreads * kContribRowsPerThread;
 
 // bf16 inputs; states in bf16, or in float32 when state_f32
 hipError_t launch_attn_bf16(const AttnArgs& a, int D, bool state_f32, hipStream_t s);
+// Bytes of workspace the tail split of a bf16 launch needs on the current
+// device (0: no split helps); `a` needs q_len, B, H and n_sel set.
+hipError_t attn_bf16_split_bytes(const AttnArgs& a, int D, size_t* bytes);
+// The same launch with a workspace: splits the tail when `ws_bytes` covers
+// attn_bf16_split_bytes, else runs unsplit.
+hipError_t launch_attn_bf16_ws(const AttnArgs& a, int D, bool state_f32, void* ws, size_t ws_bytes,
+                               hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, int D, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, ditango_dtype sdt, ditango_dtype odt, int D,
                         hipStream_t s);

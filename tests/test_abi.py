@@ -153,3 +153,32 @@ def test_attn_ex_state_dtype_validation(L):
     assert call(0, 1) == 2            # float32 inputs with bf16 states: not built
     o_bad = (ctypes.c_int64 * 3)(0, 6, 5)
     assert f(FAKE, FAKE, FAKE, 1, 1, 2, 128, 10, o_bad, 2, s, 0.1, FAKE, 0, FAKE, None) == 1
+
+
+def attn_ws(L, ws=0x1000, ws_bytes=4096, D=128, dt=1, state_dt=1, offs=(0, 5, 10), sel=(1, 1), q=FAKE):
+    P = len(offs) - 1
+    o = (ctypes.c_int64 * len(offs))(*offs)
+    s = (ctypes.c_uint8 * len(sel))(*sel)
+    return L.ditango_attn_partition_states_ws(q, FAKE, FAKE, dt, 1, 2, D, 10, o, P, s, 0.1,
+                                              FAKE, state_dt, FAKE, ws, ws_bytes, None)
+
+
+def test_attn_ws_argument_validation(L):
+    # the same checks as the other attention entry points, then the workspace
+    assert attn_ws(L, q=None) == 1
+    assert attn_ws(L, D=96) == 2
+    assert attn_ws(L, offs=(0, 6, 5)) == 1
+    assert attn_ws(L, dt=0, state_dt=1) == 2
+    assert attn_ws(L, ws=0x1000 + 64) == 1          # not 256-byte aligned
+    assert attn_ws(L, sel=(0, 0)) == 0              # nothing selected: nothing launched
+
+
+def test_attn_workspace_bytes_without_a_split(L):
+    o = (ctypes.c_int64 * 3)(0, 5, 10)
+    s = (ctypes.c_uint8 * 2)(1, 1)
+    none = (ctypes.c_uint8 * 2)(0, 0)
+    # float32 inputs never split; invalid shapes and empty selections need nothing
+    assert L.ditango_attn_workspace_bytes(0, 1, 2, 128, 10, o, 2, s) == 0
+    assert L.ditango_attn_workspace_bytes(1, 1, 2, 96, 10, o, 2, s) == 0
+    assert L.ditango_attn_workspace_bytes(1, 0, 2, 128, 10, o, 2, s) == 0
+    assert L.ditango_attn_workspace_bytes(1, 1, 2, 128, 10, o, 2, none) == 0
