@@ -403,9 +403,11 @@ def sweep(args, w):
     rows = []
     for sel in w.sweep:
         mask = [1 if j in sel else 0 for j in range(w.P)]
+        n_ws = api.attn_workspace_bytes(torch.bfloat16, w.B, w.H, w.D, L, offs, mask)
+        ws_k = torch.empty(n_ws, dtype=torch.uint8, device="cuda") if n_ws > 0 else None
 
         def step():
-            api.attn_partition_states(q, k, v, offs, mask, w.scale, st, ls)
+            api.attn_partition_states(q, k, v, offs, mask, w.scale, st, ls, ws_k)
             api.merge_states(st, ls, out, lse)
             api.contrib(ls, lse, wp, ws)
         for _ in range(args.warmup):

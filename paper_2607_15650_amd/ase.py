@@ -30,6 +30,7 @@ from typing import Dict, List, Optional, Sequence, Tuple
 import torch
 
 from . import api
+from .workspace import AttnWorkspace
 from .groups import base_groups
 
 
@@ -70,6 +71,7 @@ class ErrorModelSelectiveAttention:
         self.eps: Optional[float] = None
         nws = max(api.norms_workspace_bytes(B, H, D, self.L, self.P), api.contrib_workspace_bytes(B, H, self.L, self.P))
         self._ws = torch.empty(max(16, nws), dtype=torch.uint8, device=device)
+        self._attn_ws = AttnWorkspace(device)
 
     # ---------------------------------------------------------------- helpers
     def _norms(self, states: torch.Tensor, slots: Sequence[int], ref: Optional[torch.Tensor] = None) -> List[float]:
@@ -85,7 +87,8 @@ class ErrorModelSelectiveAttention:
         self.snap[t] = slot
 
     def _attn(self, q, k, v, sel, states, lses):
-        api.attn_partition_states(q, k, v, self.offsets, sel, self.scale, states, lses)
+        ws = self._attn_ws.get(q.dtype, q.shape[0], q.shape[2], q.shape[3], q.shape[1], self.offsets, sel)
+        api.attn_partition_states(q, k, v, self.offsets, sel, self.scale, states, lses, ws)
 
     def _compose_group(self, states, lses, grp):
         if grp[1] - grp[0] > 1:

@@ -23,6 +23,7 @@ from typing import List, Optional, Sequence, Tuple
 import torch
 
 from . import api
+from .workspace import AttnWorkspace
 
 
 def base_groups(P: int, q: int, g: int) -> List[Tuple[int, int]]:
@@ -72,6 +73,7 @@ class GroupedSelectiveAttention:
         self.L = self.offsets[q + 1] - self.offsets[q]
         self.out = torch.zeros((self.P, B, self.L, H, D), dtype=dtype, device=device)
         self.lse = torch.full((self.P, B, H, self.L), float("-inf"), dtype=torch.float32, device=device)
+        self._attn_ws = AttnWorkspace(device)
         self.budget = mem_budget_bytes
         self.groups = base_groups(self.P, q, g)
         self.computed_at = {grp: -1 for grp in self.groups}
@@ -133,7 +135,8 @@ class GroupedSelectiveAttention:
         qb = q_all[:, a:e]
         if not qb.is_contiguous():
             qb = qb.contiguous()
-        api.attn_partition_states(qb, k, v, self.offsets, sel, self.scale, self.out, self.lse)
+        ws = self._attn_ws.get(qb.dtype, self.B, self.H, self.D, self.L, self.offsets, sel)
+        api.attn_partition_states(qb, k, v, self.offsets, sel, self.scale, self.out, self.lse, ws)
         for grp in self.groups:
             if grp in compute:
                 if grp[1] - grp[0] > 1:

@@ -15,6 +15,7 @@ from typing import List, Sequence, Tuple
 import torch
 
 from . import api
+from .workspace import AttnWorkspace
 
 
 class StateCache:
@@ -47,6 +48,7 @@ class SelectiveAttention:
         self.device = device
         self.caches = {}
         self._ws = {}
+        self._attn_ws = AttnWorkspace(device)
 
     def cache(self, qb: int) -> StateCache:
         if qb not in self.caches:
@@ -66,7 +68,8 @@ class SelectiveAttention:
         q = q_all[:, a:e]
         if not q.is_contiguous():
             q = q.contiguous()
-        api.attn_partition_states(q, k, v, self.offsets, select, self.scale, c.out, c.lse)
+        ws = self._attn_ws.get(q.dtype, self.B, self.H, self.D, e - a, self.offsets, select)
+        api.attn_partition_states(q, k, v, self.offsets, select, self.scale, c.out, c.lse, ws)
         for j, s in enumerate(select):
             if s:
                 c.computed_at[j] = step
