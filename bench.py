@@ -38,8 +38,9 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # elementwise copy reads / writes 1 GiB), keyed by the build id (source and
 # compile options) of the kernel they were taken on; reported only while the
 # build id matches.
-ATTN_TRAFFIC = {"build_id": "d6bd9cf8c8e3372f", "workload": "videodit_bf16_h40_d128_s75600_p8",
-                "fetch_bytes": 746676 * 1024 * 2.0, "write_bytes": 287956 * 1024 * 1.0}
+ATTN_TRAFFIC = {"build_id": "65be59f9b9f27c75", "workload": "videodit_bf16_h40_d128_s75600_p8",
+                # the attention kernel with its last round split, plus the fix-up kernel
+                "fetch_bytes": (763431 + 45661) * 1024 * 2.0, "write_bytes": (372808 + 5747) * 1024 * 1.0}
 
 
 def parse():
@@ -88,7 +89,7 @@ def algorithmic(w, select):
 # rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_LDS_BANK_CONFLICT
 # (busy fraction = busy cycles / (1024 SIMDs x GRBM cycles / 8 XCDs); clock =
 # GRBM cycles / 8 / the traced kernel duration); reported under the same rule.
-ATTN_COUNTERS = {"mfma_busy": 0.596, "lds_bank_conflicts": 0, "clock_ghz": 1.78}
+ATTN_COUNTERS = {"mfma_busy": 0.615, "lds_bank_conflicts": 0, "clock_ghz": 1.77}
 
 
 # HBM bytes per launch of the merge kernel at the default workload (all P
@@ -105,16 +106,16 @@ def merge_traffic(w):
     return MERGE_TRAFFIC["fetch_bytes"] + MERGE_TRAFFIC["write_bytes"]
 
 
-def attn_counters(w, select):
-    return dict(ATTN_COUNTERS) if attn_traffic(w, select) is not None else None
+def attn_counters(w, select, split):
+    return dict(ATTN_COUNTERS) if attn_traffic(w, select, split) is not None else None
 
 
-def attn_traffic(w, select):
+def attn_traffic(w, select, split):
     """Profiled HBM bytes per attention launch, or None when the kernel build,
-    the workload or the selection differs from the one the counters were
-    taken on."""
+    the workload, the selection or the use of the tail split differs from the
+    one the counters were taken on."""
     from paper_2607_15650_amd import build
-    if build.source_id("attn_bf16.hip") != ATTN_TRAFFIC["build_id"]:
+    if build.source_id("attn_bf16.hip") != ATTN_TRAFFIC["build_id"] or not split:
         return None
     if w.name != ATTN_TRAFFIC["workload"] or tuple(select) != w.select:
         return None
@@ -656,9 +657,12 @@ def main():
                    "query_partition": w.q, "q_len": q_len, "fresh_partitions": list(select),
                    "fresh_fraction": len(select) / w.P,
                    "attn_workspace_bytes": int(ws_attn.numel()) if ws_attn is not None else 0},
-        "roofline": {"bound": "mfma", "kernel": "attn_bf16_kernel" if w.dtype == "bf16" else "attn_f32_kernel",
+        "roofline": {"bound": "mfma",
+                     "kernel": ("attn_bf16_kernel" + (" + attn_split_fixup_kernel" if ws_attn is not None else ""))
+                     if w.dtype == "bf16" else "attn_f32_kernel",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": attn_traffic(w, select), "counters": attn_counters(w, select)},
+                     "traffic": attn_traffic(w, select, ws_attn is not None),
+                     "counters": attn_counters(w, select, ws_attn is not None)},
         "kernels_ms": {"attn_partition_states": {"mean": attn_ms, "median": med(t_attn)},
                        "merge_states": {"mean": merge_ms, "median": med(t_merge)},
                        "contrib": {"mean": mean(t_contrib), "median": med(t_contrib)}},
