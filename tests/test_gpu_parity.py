@@ -43,8 +43,13 @@ def run_step(w, x, select, rows_prev=True):
     if "q_prev" in dev:
         a.attn_partition_states(dev["q_prev"][:, qa:qb].contiguous(), dev["k_prev"], dev["v_prev"],
                                 offs, [1] * P, w.scale, out_states, lse_states)
-    a.attn_partition_states(dev["q"][:, qa:qb].contiguous(), dev["k"], dev["v"], offs,
-                            [1 if j in select else 0 for j in range(P)], w.scale, out_states, lse_states)
+    # the current step as bench.py launches it: with the workspace that splits
+    # the launch's last round when that shortens it
+    mask = [1 if j in select else 0 for j in range(P)]
+    n_ws = a.attn_workspace_bytes(torch_dtype(w.dtype), w.B, w.H, w.D, q_len, offs, mask)
+    ws_attn = torch.empty(n_ws, dtype=torch.uint8, device="cuda") if n_ws > 0 else None
+    a.attn_partition_states(dev["q"][:, qa:qb].contiguous(), dev["k"], dev["v"], offs, mask, w.scale,
+                            out_states, lse_states, ws_attn)
     out = torch.empty((w.B, q_len, w.H, w.D), dtype=torch_dtype(w.dtype), device="cuda")
     lse = torch.empty((w.B, w.H, q_len), dtype=torch.float32, device="cuda")
     a.merge_states(out_states, lse_states, out, lse)
