@@ -38,7 +38,7 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # elementwise copy reads / writes 1 GiB), keyed by the build id (source and
 # compile options) of the kernel they were taken on; reported only while the
 # build id matches.
-ATTN_TRAFFIC = {"build_id": "65be59f9b9f27c75", "workload": "videodit_bf16_h40_d128_s75600_p8",
+ATTN_TRAFFIC = {"build_id": "65be59f9b9f27c75", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "split",
                 # the attention kernel with its last round split, plus the fix-up kernel
                 "fetch_bytes": (763431 + 45661) * 1024 * 2.0, "write_bytes": (372808 + 5747) * 1024 * 1.0}
 
@@ -61,8 +61,9 @@ def parse():
     ap.add_argument("--eps-local", type=float, default=0.1)
     ap.add_argument("--sweep", action="store_true",
                     help="time the step for each selection of the workload's sweep (long-context workload)")
-    ap.add_argument("--no-tail-split", dest="tail_split", action="store_false",
-                    help="launch the attention kernel without the workspace that splits its last round")
+    ap.add_argument("--attn-workspace", choices=("full", "queue", "none"), default="full",
+                    help="workspace of the attention launch: queue counters and tail-split partials (full), "
+                         "the queue counters only (balanced, unsplit), or none (static launch)")
     ap.add_argument("--no-selection-sweep", dest="selection_sweep", action="store_false",
                     help="skip the step-time-against-selected-fraction points")
     ap.add_argument("--power-seconds", type=float, default=3.0,
@@ -106,16 +107,30 @@ def merge_traffic(w):
     return MERGE_TRAFFIC["fetch_bytes"] + MERGE_TRAFFIC["write_bytes"]
 
 
-def attn_counters(w, select, split):
-    return dict(ATTN_COUNTERS) if attn_traffic(w, select, split) is not None else None
+def attn_mode(ws):
+    """How the attention launch runs with this workspace: "static" (none),
+    "queue" (balanced over the XCDs) or "split" (balanced, last round split)."""
+    if ws is None:
+        return "static"
+    return "split" if ws.numel() > 256 else "queue"
 
 
-def attn_traffic(w, select, split):
+def attn_kernels(ws):
+    mode = attn_mode(ws)
+    return {"static": "attn_bf16_kernel", "queue": "attn_queue_reset_kernel + attn_bf16_kernel",
+            "split": "attn_queue_reset_kernel + attn_bf16_kernel + attn_split_fixup_kernel"}[mode]
+
+
+def attn_counters(w, select, mode):
+    return dict(ATTN_COUNTERS) if attn_traffic(w, select, mode) is not None else None
+
+
+def attn_traffic(w, select, mode):
     """Profiled HBM bytes per attention launch, or None when the kernel build,
-    the workload, the selection or the use of the tail split differs from the
-    one the counters were taken on."""
+    the workload, the selection or the launch mode differs from the one the
+    counters were taken on."""
     from paper_2607_15650_amd import build
-    if build.source_id("attn_bf16.hip") != ATTN_TRAFFIC["build_id"] or not split:
+    if build.source_id("attn_bf16.hip") != ATTN_TRAFFIC["build_id"] or mode != ATTN_TRAFFIC["mode"]:
         return None
     if w.name != ATTN_TRAFFIC["workload"] or tuple(select) != w.select:
         return None
@@ -495,10 +510,15 @@ def main():
     lse = torch.empty((w.B, w.H, q_len), dtype=torch.float32, device="cuda")
     w_part = torch.empty(w.P, dtype=torch.float32, device="cuda")
     ws = torch.empty(max(16, api.contrib_workspace_bytes(w.B, w.H, q_len, w.P)), dtype=torch.uint8, device="cuda")
-    # workspace of the attention launch: lets it split the tasks of a partly
-    # filled last round over key ranges (None when no split helps)
+    # workspace of the attention launch: queue counters that balance its
+    # last tasks over the XCDs, and room to split the tasks of a partly
+    # filled last round over key ranges (None: the static launch)
     def attn_ws(sel_mask):
-        n = api.attn_workspace_bytes(dt, w.B, w.H, w.D, q_len, offs, sel_mask) if args.tail_split else 0
+        if args.attn_workspace == "none":
+            return None
+        n = api.attn_workspace_bytes(dt, w.B, w.H, w.D, q_len, offs, sel_mask)
+        if args.attn_workspace == "queue":
+            n = min(n, 256)
         return torch.empty(n, dtype=torch.uint8, device="cuda") if n > 0 else None
     ws_attn = attn_ws(mask)
 
@@ -656,13 +676,13 @@ def main():
         "config": {"workload": w.name, "B": w.B, "H": w.H, "D": w.D, "S": w.S, "P": w.P,
                    "query_partition": w.q, "q_len": q_len, "fresh_partitions": list(select),
                    "fresh_fraction": len(select) / w.P,
+                   "attn_launch": attn_mode(ws_attn),
                    "attn_workspace_bytes": int(ws_attn.numel()) if ws_attn is not None else 0},
         "roofline": {"bound": "mfma",
-                     "kernel": ("attn_bf16_kernel" + (" + attn_split_fixup_kernel" if ws_attn is not None else ""))
-                     if w.dtype == "bf16" else "attn_f32_kernel",
+                     "kernel": attn_kernels(ws_attn) if w.dtype == "bf16" else "attn_f32_kernel",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": attn_traffic(w, select, ws_attn is not None),
-                     "counters": attn_counters(w, select, ws_attn is not None)},
+                     "traffic": attn_traffic(w, select, attn_mode(ws_attn)),
+                     "counters": attn_counters(w, select, attn_mode(ws_attn))},
         "kernels_ms": {"attn_partition_states": {"mean": attn_ms, "median": med(t_attn)},
                        "merge_states": {"mean": merge_ms, "median": med(t_merge)},
                        "contrib": {"mean": mean(t_contrib), "median": med(t_contrib)}},

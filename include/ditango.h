@@ -103,25 +103,32 @@ ditango_status ditango_attn_partition_states_ex(
     void* out_states, ditango_dtype state_dt, float* lse_states, void* stream);
 
 /*
- * The same with a workspace that lets the launch balance its last round
- * (the same computation, Sec. 2.2.4, Eq. attention_state; the partial states
- * are composed by Eq. composition).  A launch is a set of equal-length tasks
- * (query tile x head x batch x selected partition) of which the GPU runs a
- * fixed number at a time; the tasks of a last, partly filled round are each
- * split into up to 8 key ranges whose partial states go to the workspace and
- * are composed into their slots by a second, small kernel on `stream`.
+ * The same with a workspace that lets the launch balance its work over the
+ * XCDs and shorten its last round (the same computation, Sec. 2.2.4, Eq.
+ * attention_state; split partial states are composed by Eq. composition).
+ * A launch is a set of tasks (query tile x head x batch x selected
+ * partition) of which the GPU runs a fixed number at a time.
+ *  - Balancing: the first 256 bytes of the workspace hold queue counters
+ *    (zeroed by a small kernel on `stream` before the launch).  Most tasks
+ *    run where the hardware places them; the last ones are claimed from the
+ *    counters, so that XCDs that run faster take more of them.
+ *  - Tail split: when the last round is partly filled, its tasks are split
+ *    into up to 8 key ranges whose partial states go to the rest of the
+ *    workspace and are composed into their slots by a second small kernel.
  *
- *   workspace        device, 256-byte aligned, at least
- *                    ditango_attn_workspace_bytes(...) bytes for this shape and
- *                    selection on the current device; NULL or fewer bytes:
- *                    the launch runs unsplit (the result of
- *                    ditango_attn_partition_states_ex).  Contents on entry
- *                    are ignored; on return they are scratch.  Calls that
- *                    overlap on one workspace race.
+ *   workspace        device, 256-byte aligned.  NULL or under 256 bytes:
+ *                    the static launch of ditango_attn_partition_states_ex;
+ *                    at least 256: balanced; at least
+ *                    ditango_attn_workspace_bytes(...) for this shape and
+ *                    selection on the current device: balanced and split.
+ *                    Contents on entry are ignored; on return they are
+ *                    scratch.  Calls that overlap on one workspace race.
  *   workspace_bytes  its size.
  *
- * Split results differ from unsplit ones only by the rounding of the
- * composition; both are deterministic.  fp32 inputs never split.
+ * Balancing moves tasks between workgroups, not their arithmetic: a
+ * balanced unsplit launch is bitwise the static one.  Split results differ
+ * from unsplit ones only by the rounding of the composition; all are
+ * deterministic.  fp32 inputs ignore the workspace.
  * DITANGO_ERR_INVALID for a misaligned workspace; otherwise as
  * ditango_attn_partition_states_ex.
  */
@@ -133,10 +140,11 @@ ditango_status ditango_attn_partition_states_ws(
     void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * Workspace bytes ditango_attn_partition_states_ws needs to split the last
- * round of this launch on the current HIP device (its compute-unit count and
- * the kernel's occupancy decide); 0 when no split shortens it, for fp32
- * inputs, or for invalid arguments.  Host only, enqueues nothing.
+ * Workspace bytes ditango_attn_partition_states_ws uses for this launch on
+ * the current HIP device: 256 for the queue counters, plus the partial
+ * states of the tail split when a split shortens the last round (the
+ * compute-unit count and the kernel's occupancy decide).  0 for fp32 inputs,
+ * an empty selection or invalid arguments.  Host only, enqueues nothing.
  */
 size_t ditango_attn_workspace_bytes(ditango_dtype dt, int B, int H, int D, int64_t q_len,
                                     const int64_t* kv_offsets, int P, const uint8_t* select);

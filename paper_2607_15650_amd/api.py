@@ -53,8 +53,10 @@ def _stream() -> int:
 
 def attn_workspace_bytes(dtype: torch.dtype, B: int, H: int, D: int, q_len: int,
                          offsets: Sequence[int], select: Sequence[int]) -> int:
-    """Workspace bytes that let attn_partition_states split its last round
-    on the current device (ditango_attn_workspace_bytes); 0 = no split helps."""
+    """Workspace bytes attn_partition_states uses for this launch on the
+    current device (ditango_attn_workspace_bytes): 256 for the queue counters
+    that balance the launch over the XCDs, plus the partial states of the
+    tail split when a split shortens the last round; 0 for float32 inputs."""
     P = len(offsets) - 1
     offs = (ctypes.c_int64 * (P + 1))(*[int(x) for x in offsets])
     sel = (ctypes.c_uint8 * P)(*[1 if s else 0 for s in select])
@@ -69,9 +71,10 @@ def attn_partition_states(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
     (ditango_attn_partition_states).  Unselected slots are left untouched.
     ``out_states`` is in the input dtype, or float32 for bf16 inputs
     (ditango_attn_partition_states_ex: states at full precision).  With a
-    ``workspace`` (uint8, attn_workspace_bytes(...) bytes, 256-byte aligned)
-    the last round of the launch is split over key ranges
-    (ditango_attn_partition_states_ws)."""
+    ``workspace`` (uint8, 256-byte aligned; ditango_attn_partition_states_ws)
+    the last tasks are claimed from queue counters in its first 256 bytes,
+    and with attn_workspace_bytes(...) bytes the last round is split over
+    key ranges as well."""
     _dev(q, k, v, out_states, lse_states, workspace)
     B, q_len, H, D = q.shape
     P = len(offsets) - 1

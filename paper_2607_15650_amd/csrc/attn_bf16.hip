@@ -157,20 +157,82 @@ __device__ __forceinline__ void store4(__bf16* p, const f32x4& x) {
 }
 __device__ __forceinline__ void store4(float* p, const f32x4& x) { *(f32x4*)p = x; }
 
+// Claims one unit of work from the queue counters for a workgroup past the
+// static ones (called by all 64 lanes of its first wave; the result is
+// wave-uniform).  Units: a main task id, or n_main + u for split unit u.
+// Order: this XCD's own queue; then, from one look at all the counters, the
+// main queue with the most units left, else the split queue; finally every
+// queue in turn.  Counters only grow, so a queue seen exhausted stays so, and
+// -1 (nothing left) is returned only after every queue was seen exhausted.
+__device__ int claim_unit(const AttnArgs& a, int lane) {
+  unsigned xcc;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+  const int own = (int)(xcc & 7);
+  const int s = a.n_static >> 3;
+  const int n_tail = a.n_split * a.split_f;
+  auto qlen = [&](int q) { return q < 8 ? xcd_len(q, a.n_main) - s : (q == 8 ? n_tail : 0); };
+  // one atomic increment of queue q (wave-uniform) by lane 0
+  auto take = [&](int q) -> int {
+    const int len = qlen(q);
+    if (len <= 0) return -1;
+    int t = 0;
+    if (lane == 0) t = __hip_atomic_fetch_add(a.queue + q, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    t = __builtin_amdgcn_readfirstlane(t);
+    if (t >= len) return -1;
+    return q < 8 ? xcd_first(q, a.n_main) + s + t : a.n_main + t;
+  };
+  int u = take(own);
+  if (u >= 0) return u;
+  for (int it = 0; it < 4; ++it) {
+    int left = 0;
+    if (lane < 9) left = qlen(lane) - __hip_atomic_load(a.queue + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // main queue with the most left: max over lanes 0..7 of (left, lane)
+    int key = (lane < 8 && left > 0) ? (left << 3) | lane : -1;
+    key = max(key, __shfl_xor(key, 1));
+    key = max(key, __shfl_xor(key, 2));
+    key = max(key, __shfl_xor(key, 4));
+    key = __builtin_amdgcn_readfirstlane(key);
+    const int tail_left = __builtin_amdgcn_readlane(left, 8);
+    int q;
+    if (key >= 0) q = key & 7;
+    else if (tail_left > 0) q = 8;
+    else return -1;
+    u = take(q);
+    if (u >= 0) return u;
+  }
+  for (int k = 1; k <= 8; ++k) {
+    u = take(k < 8 ? (own + k) & 7 : 8);
+    if (u >= 0) return u;
+  }
+  return -1;
+}
+
 template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
 __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs a) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
-  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];   // 2*NBUF tiles
+  // 2*NBUF tiles, then one int: the claimed unit of a queue workgroup
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
 
   // ---- task decode: (selected partition, batch, head, query tile), and for
   // a task of the split tail, which of its split_f key ranges
   int task, part = -1;
-  if ((int)blockIdx.x < a.n_main) {
-    task = xcd_remap(blockIdx.x, a.n_main);
+  if ((int)blockIdx.x < a.n_static) {
+    task = xcd_first((int)blockIdx.x & 7, a.n_main) + ((int)blockIdx.x >> 3);
   } else {
-    const int u = (int)blockIdx.x - a.n_main;
-    task = a.n_main + u / a.split_f;
-    part = u % a.split_f;
+    int* claimed = (int*)(smem + 2 * NBUF * C::TILEB);
+    if (threadIdx.x < 64) {
+      const int u = claim_unit(a, (int)threadIdx.x);
+      if (threadIdx.x == 0) *claimed = u;
+    }
+    __syncthreads();
+    const int u = __builtin_amdgcn_readfirstlane(*claimed);
+    if (u < 0) return;
+    if (u < a.n_main) {
+      task = u;
+    } else {
+      task = a.n_main + (u - a.n_main) / a.split_f;
+      part = (u - a.n_main) % a.split_f;
+    }
   }
   const int qt = task % a.q_tiles;
   int t = task / a.q_tiles;
@@ -588,72 +650,108 @@ __global__ __launch_bounds__(256) void attn_split_fixup_kernel(const AttnArgs a)
 
 constexpr size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Tail split plan of one launch: the split factor, the number of split
-// tasks and the workspace bytes (partial OUT in float32, then partial LSE).
+// Zeroes the queue counters of a balanced launch (a kernel, not a memset, so
+// that the launch sequence can be captured in a graph).
+__global__ __launch_bounds__(64) void attn_queue_reset_kernel(int* queue) {
+  if (threadIdx.x < kQueueInts) queue[threadIdx.x] = 0;
+}
+
+// Dynamic share of the balanced launch: the last DITANGO_DYN_ROUNDS rounds of
+// resident workgroups of every XCD's range are claimed from the queues.
+#ifndef DITANGO_DYN_ROUNDS
+#define DITANGO_DYN_ROUNDS 2
+#endif
+
+// Launch plan of one bf16 launch: resident workgroup slots on the current
+// device, the tail split factor and number of split tasks, and the workspace
+// bytes (queue counters, partial OUT in float32, partial LSE).
+struct Plan {
+  int64_t slots = 0;
+  int f = 1;
+  int64_t n_split = 0;
+  size_t split_bytes = 0;   // partial states
+  size_t bytes = 0;         // kQueueBytes + split_bytes (0: nothing launched)
+};
+
 template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
-hipError_t plan_cfg(const AttnArgs& a, int* f_out, int64_t* n_split_out, size_t* bytes_out) {
-  using C = Cfg<D, QB, NW, BN, NBUF>;
-  const size_t lds = (size_t)2 * NBUF * C::TILEB;
+hipError_t set_lds(size_t lds) {
   static const hipError_t attr = hipFuncSetAttribute(
       (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>,
       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (attr != hipSuccess) return attr;
-  *f_out = 1;
-  *n_split_out = 0;
-  *bytes_out = 0;
+  return attr;
+}
+
+template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
+hipError_t plan_cfg(const AttnArgs& a, Plan* p) {
+  using C = Cfg<D, QB, NW, BN, NBUF>;
+  const size_t lds = (size_t)2 * NBUF * C::TILEB + 16;
+  hipError_t e = set_lds<D, QB, NW, BN, NBUF, WPE, SEQ, TS>(lds);
+  if (e != hipSuccess) return e;
+  *p = Plan{};
   const int64_t nblk = (a.q_len + C::BM - 1) / C::BM * a.H * a.B * a.n_sel;
   if (nblk <= 0) return hipSuccess;
   int dev = 0, cus = 0, occ = 0;
-  hipError_t e = hipGetDevice(&dev);
+  e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e == hipSuccess)
     e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
         &occ, (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>, C::NT, lds);
   if (e != hipSuccess) return e;
-  const int64_t slots = (int64_t)cus * (occ > 0 ? occ : 1);
-  const int f = plan_tail_split(nblk, slots);
+  p->slots = (int64_t)cus * (occ > 0 ? occ : 1);
+  p->bytes = kQueueBytes;
+  const int f = plan_tail_split(nblk, p->slots);
   if (f <= 1) return hipSuccess;
-  const int64_t n_split = nblk % slots;
-  *f_out = f;
-  *n_split_out = n_split;
-  *bytes_out = align256((size_t)n_split * f * C::BM * D * sizeof(float)) +
-               align256((size_t)n_split * f * C::BM * sizeof(float));
+  p->f = f;
+  p->n_split = nblk % p->slots;
+  p->split_bytes = align256((size_t)p->n_split * f * C::BM * D * sizeof(float)) +
+                   align256((size_t)p->n_split * f * C::BM * sizeof(float));
+  p->bytes += p->split_bytes;
   return hipSuccess;
 }
 
 template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
 hipError_t launch_cfg(const AttnArgs& a0, void* ws, size_t ws_bytes, hipStream_t s) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
-  const size_t lds = (size_t)2 * NBUF * C::TILEB;
-  int f = 1;
-  int64_t n_split = 0;
-  size_t need = 0;
-  if (ws != nullptr) {
-    const hipError_t e = plan_cfg<D, QB, NW, BN, NBUF, WPE, SEQ, TS>(a0, &f, &n_split, &need);
+  const size_t lds = (size_t)2 * NBUF * C::TILEB + 16;
+  Plan p;
+  const bool queued = ws != nullptr && ws_bytes >= kQueueBytes;
+  if (queued) {
+    const hipError_t e = plan_cfg<D, QB, NW, BN, NBUF, WPE, SEQ, TS>(a0, &p);
     if (e != hipSuccess) return e;
   } else {
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>,
-        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (attr != hipSuccess) return attr;
+    const hipError_t e = set_lds<D, QB, NW, BN, NBUF, WPE, SEQ, TS>(lds);
+    if (e != hipSuccess) return e;
   }
   AttnArgs a = a0;
   a.q_tiles = (int)((a.q_len + C::BM - 1) / C::BM);
   const int64_t nblk = (int64_t)a.q_tiles * a.H * a.B * a.n_sel;
   if (nblk <= 0) return hipSuccess;
-  if (nblk + (int64_t)kMaxSplit * n_split > 0x7fffffff) return hipErrorInvalidConfiguration;
+  if (nblk + (int64_t)kMaxSplit * p.n_split + p.slots > 0x7fffffff) return hipErrorInvalidConfiguration;
+  a.n_main = (int)nblk;
+  a.n_split = 0;
+  a.split_f = 1;
+  a.n_static = (int)nblk;
+  a.queue = nullptr;
   int64_t grid = nblk;
-  if (f > 1 && n_split > 0 && ws_bytes >= need) {
-    a.n_main = (int)(nblk - n_split);
-    a.n_split = (int)n_split;
-    a.split_f = f;
-    a.part_out = (float*)ws;
-    a.part_lse = (float*)((char*)ws + align256((size_t)n_split * f * C::BM * D * sizeof(float)));
-    grid = a.n_main + n_split * f;
-  } else {
-    a.n_main = (int)nblk;
-    a.n_split = 0;
-    a.split_f = 1;
+  if (queued) {
+    a.queue = (int*)ws;
+    if (p.f > 1 && ws_bytes >= p.bytes) {
+      a.n_main = (int)(nblk - p.n_split);
+      a.n_split = (int)p.n_split;
+      a.split_f = p.f;
+      a.part_out = (float*)((char*)ws + kQueueBytes);
+      a.part_lse = (float*)((char*)a.part_out + align256((size_t)p.n_split * p.f * C::BM * D * sizeof(float)));
+    }
+    // static share: all but the last DITANGO_DYN_ROUNDS rounds of every
+    // XCD's range; one extra round of workgroups lets the faster XCDs take
+    // units from the slower ones' queues
+    const int64_t per_xcd_slots = p.slots / 8 > 0 ? p.slots / 8 : 1;
+    const int64_t st = (int64_t)(a.n_main / 8) - DITANGO_DYN_ROUNDS * per_xcd_slots;
+    a.n_static = st > 0 ? (int)(8 * st) : 0;
+    grid = (int64_t)a.n_main + (int64_t)a.n_split * a.split_f + 8 * per_xcd_slots;
+    hipLaunchKernelGGL(attn_queue_reset_kernel, dim3(1), dim3(64), 0, s, a.queue);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>), dim3((unsigned)grid), dim3(C::NT), lds,
                      s, a);
@@ -696,15 +794,16 @@ hipError_t launch_attn_bf16(const AttnArgs& a, int D, bool state_f32, hipStream_
   return launch_attn_bf16_ws(a, D, state_f32, nullptr, 0, s);
 }
 
-hipError_t attn_bf16_split_bytes(const AttnArgs& a, int D, size_t* bytes) {
-  int f = 1;
-  int64_t n_split = 0;
+hipError_t attn_bf16_ws_bytes(const AttnArgs& a, int D, size_t* bytes) {
+  Plan p;
   *bytes = 0;
   // the plan depends on the kernel's occupancy, which the state type does
   // not change; the bf16-state instantiation is queried
-  if (D == 128) return plan_cfg<128, DITANGO_D128_CFG, __bf16>(a, &f, &n_split, bytes);
-  if (D == 64) return plan_cfg<64, DITANGO_D64_CFG, __bf16>(a, &f, &n_split, bytes);
-  return hipErrorInvalidValue;
+  hipError_t e = hipErrorInvalidValue;
+  if (D == 128) e = plan_cfg<128, DITANGO_D128_CFG, __bf16>(a, &p);
+  if (D == 64) e = plan_cfg<64, DITANGO_D64_CFG, __bf16>(a, &p);
+  if (e == hipSuccess) *bytes = p.bytes;
+  return e;
 }
 
 }  // namespace ditango

@@ -124,7 +124,7 @@ size_t ditango_attn_workspace_bytes(ditango_dtype dt, int B, int H, int D, int64
                 (const float*)dummy, &a) != DITANGO_OK || a.n_sel == 0)
     return 0;
   size_t bytes = 0;
-  if (attn_bf16_split_bytes(a, D, &bytes) != hipSuccess) return 0;
+  if (attn_bf16_ws_bytes(a, D, &bytes) != hipSuccess) return 0;
   return bytes;
 }
 

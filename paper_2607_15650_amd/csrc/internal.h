@@ -37,9 +37,22 @@ struct AttnArgs {
   int split_f;
   float* part_out;          // [n_split * split_f][rows per workgroup][D]
   float* part_lse;          // [n_split * split_f][rows per workgroup]
+  // Balancing over the XCDs (bf16 kernel, with a workspace).  The main tasks
+  // are cut into 8 contiguous ranges, one per XCD (xcd_first / xcd_len).
+  // Workgroups [0, n_static) run fixed tasks: workgroup b the (b / 8)-th
+  // task of range b % 8.  Every later workgroup claims one unit from the
+  // queue counters: queue x < 8 holds the rest of range x, queue 8 the
+  // n_split * split_f split units; its own XCD's queue first, then the main
+  // queue with the most left, then the split queue; it exits when all are
+  // exhausted.  queue = null: no queues, every workgroup is static
+  // (n_static = n_main).
+  int n_static;
+  int* queue;               // kQueueInts counters, zeroed before the launch
 };
 
 constexpr int kMaxSplit = 8;
+constexpr int kQueueInts = 16;
+constexpr size_t kQueueBytes = 256;   // the queue counters, at the start of the workspace
 
 // Tail split plan: with `slots` workgroups resident at once and `tasks`
 // equal-length tasks, the last round runs tasks % slots of them; splitting
@@ -106,11 +119,13 @@ constexpr int kContribRowsPerBlock = kContribThreads * kContribRowsPerThread;
 
 // bf16 inputs; states in bf16, or in float32 when state_f32
 hipError_t launch_attn_bf16(const AttnArgs& a, int D, bool state_f32, hipStream_t s);
-// Bytes of workspace the tail split of a bf16 launch needs on the current
-// device (0: no split helps); `a` needs q_len, B, H and n_sel set.
-hipError_t attn_bf16_split_bytes(const AttnArgs& a, int D, size_t* bytes);
-// The same launch with a workspace: splits the tail when `ws_bytes` covers
-// attn_bf16_split_bytes, else runs unsplit.
+// Bytes of workspace a bf16 launch uses on the current device: the queue
+// counters, and the partial states of the tail split when a split shortens
+// the last round (0: nothing is launched); `a` needs q_len, B, H and n_sel.
+hipError_t attn_bf16_ws_bytes(const AttnArgs& a, int D, size_t* bytes);
+// The same launch with a workspace: balanced over the XCDs when `ws_bytes`
+// covers the queue counters, and with the tail split as well when it covers
+// attn_bf16_ws_bytes; a null workspace runs the static assignment.
 hipError_t launch_attn_bf16_ws(const AttnArgs& a, int D, bool state_f32, void* ws, size_t ws_bytes,
                                hipStream_t s);
 hipError_t launch_attn_f32(const AttnArgs& a, int D, hipStream_t s);
@@ -127,6 +142,9 @@ hipError_t launch_probe_mfma(int n_workgroups, int iters, float* sink, hipStream
 // b % 8.  The remap gives every XCD a contiguous run of logical task ids, so
 // tasks that read the same key/value rows (consecutive query tiles of one
 // head and partition) share that XCD's L2.
+__device__ __forceinline__ int xcd_first(int x, int n) { return x * (n >> 3) + min(x, n & 7); }
+__device__ __forceinline__ int xcd_len(int x, int n) { return (n >> 3) + (x < (n & 7) ? 1 : 0); }
+
 __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   constexpr int kXcd = 8;
   const int per = nblocks / kXcd;

@@ -1,7 +1,8 @@
-"""Device workspace of the attention launch's tail split, kept across calls.
+"""Device workspace of the attention launch, kept across calls.
 
-ditango_attn_partition_states_ws balances a launch's last, partly filled
-round when given enough workspace; the bytes depend on the shape, the
+ditango_attn_partition_states_ws balances a launch over the XCDs with queue
+counters in the workspace, and splits its last, partly filled round when
+given room for the partial states; the bytes depend on the shape, the
 selection and the device.  This holder asks the library for them once per
 (shape, selection) and keeps one device buffer that only grows.
 """
@@ -22,7 +23,7 @@ class AttnWorkspace:
 
     def get(self, dtype: torch.dtype, B: int, H: int, D: int, q_len: int,
             offsets: Sequence[int], select: Sequence[int]) -> Optional[torch.Tensor]:
-        """The buffer for this launch, or None when no split helps."""
+        """The buffer for this launch, or None for float32 inputs."""
         key = (dtype, B, H, D, q_len, tuple(int(o) for o in offsets), tuple(1 if s else 0 for s in select))
         n = self._bytes.get(key)
         if n is None:

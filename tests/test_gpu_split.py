@@ -74,13 +74,16 @@ def test_tail_split_matches_oracle_and_unsplit(D, lens, select, state_dt):
     s_split, l_split = launch(ws)
     s_again, l_again = launch(ws)
     s_plain, l_plain = launch(None)
-    s_small, l_small = launch(ws[: need // 2])        # too small: runs unsplit
+    s_small, l_small = launch(ws[: need // 2])        # too small to split: balanced, unsplit
+    s_queue, l_queue = launch(ws[:256])                # the queue counters only
 
-    # bitwise: the split launch repeats; a short workspace is the unsplit launch
+    # bitwise: the split launch repeats; a short workspace balances without
+    # splitting, which is the static launch's arithmetic
     assert torch.equal(s_split.view(torch.uint8), s_again.view(torch.uint8))
     assert torch.equal(l_split.view(torch.int32), l_again.view(torch.int32))
-    assert torch.equal(s_small.view(torch.uint8), s_plain.view(torch.uint8))
-    assert torch.equal(l_small.view(torch.int32), l_plain.view(torch.int32))
+    for s_b, l_b in ((s_small, l_small), (s_queue, l_queue)):
+        assert torch.equal(s_b.view(torch.uint8), s_plain.view(torch.uint8))
+        assert torch.equal(l_b.view(torch.int32), l_plain.view(torch.int32))
     # unselected slots untouched
     ity = torch.int16 if sdt == torch.bfloat16 else torch.int32
     for j in range(P):
@@ -112,5 +115,6 @@ def test_no_split_when_the_last_round_is_full():
     if q_tiles * H != 2 * cus:
         pytest.skip("compute-unit count not a multiple of 8")
     q_len = q_tiles * ROWS[128]
-    assert a.attn_workspace_bytes(torch.bfloat16, 1, H, 128, q_len, [0, 640], [1]) == 0
+    # the queue counters only; fp32 inputs use no workspace
+    assert a.attn_workspace_bytes(torch.bfloat16, 1, H, 128, q_len, [0, 640], [1]) == 256
     assert a.attn_workspace_bytes(torch.float32, 1, H, 128, q_len + 1, [0, 640], [1]) == 0
