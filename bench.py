@@ -38,9 +38,11 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # elementwise copy reads / writes 1 GiB), keyed by the build id (source and
 # compile options) of the kernel they were taken on; reported only while the
 # build id matches.
-ATTN_TRAFFIC = {"build_id": "65be59f9b9f27c75", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "split",
-                # the attention kernel with its last round split, plus the fix-up kernel
-                "fetch_bytes": (763431 + 45661) * 1024 * 2.0, "write_bytes": (372808 + 5747) * 1024 * 1.0}
+ATTN_TRAFFIC = {"build_id": "621957311b2f5532", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "split",
+                # the balanced attention kernel with its last round split (mean
+                # of 5 launches: stolen tasks change the bytes by +-0.5 %), plus
+                # the fix-up kernel; the queue reset moves about 1 KiB
+                "fetch_bytes": (799561 + 45661) * 1024 * 2.0, "write_bytes": (372872 + 5747) * 1024 * 1.0}
 
 
 def parse():
@@ -90,13 +92,13 @@ def algorithmic(w, select):
 # rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_LDS_BANK_CONFLICT
 # (busy fraction = busy cycles / (1024 SIMDs x GRBM cycles / 8 XCDs); clock =
 # GRBM cycles / 8 / the traced kernel duration); reported under the same rule.
-ATTN_COUNTERS = {"mfma_busy": 0.615, "lds_bank_conflicts": 0, "clock_ghz": 1.77}
+ATTN_COUNTERS = {"mfma_busy": 0.625, "lds_bank_conflicts": 0, "clock_ghz": 1.84}
 
 
 # HBM bytes per launch of the merge kernel at the default workload (all P
 # slots), from the same two counter runs and scaled the same way; reported
 # only while merge.hip's build id matches.
-MERGE_TRAFFIC = {"build_id": "86e5c5660225d068", "workload": "videodit_bf16_h40_d128_s75600_p8",
+MERGE_TRAFFIC = {"build_id": "be585a19fcc12c2b", "workload": "videodit_bf16_h40_d128_s75600_p8",
                  "fetch_bytes": 401743.5 * 1024 * 2.0, "write_bytes": 100409 * 1024 * 1.0}
 
 
