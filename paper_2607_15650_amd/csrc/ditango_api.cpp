@@ -174,8 +174,7 @@ ditango_status ditango_merge_states(
 size_t ditango_contrib_workspace_bytes(int B, int H, int64_t q_len, int P) {
   if (B < 1 || H < 1 || q_len < 1 || P < 1) return 0;
   const int64_t n_rows = (int64_t)B * H * q_len;
-  const int64_t n_blocks = (n_rows + kContribRowsPerBlock - 1) / kContribRowsPerBlock;
-  return (size_t)(n_blocks * P * (int64_t)sizeof(float));
+  return (size_t)(contrib_blocks(n_rows) * P * (int64_t)sizeof(float));
 }
 
 ditango_status ditango_contrib(
@@ -195,7 +194,7 @@ ditango_status ditango_contrib(
   a.partial = (float*)workspace;
   a.n_rows = (int64_t)B * H * q_len;
   a.P = P;
-  const int64_t nb = (a.n_rows + kContribRowsPerBlock - 1) / kContribRowsPerBlock;
+  const int64_t nb = contrib_blocks(a.n_rows);
   if (nb > 0x7fffffffLL) return DITANGO_ERR_UNSUPPORTED;
   a.n_blocks = (int)nb;
   return from_hip(launch_contrib(a, (hipStream_t)stream));

@@ -112,10 +112,9 @@ struct NormArgs {
 constexpr int kNormThreads = 256;
 constexpr int kNormChunksPerBlock = kNormThreads * 16;   // 8-element chunks per workgroup
 
-// Rows of the composed-LSE array one contrib workgroup reduces.
-constexpr int kContribThreads = 256;
-constexpr int kContribRowsPerThread = 8;
-constexpr int kContribRowsPerBlock = kContribThreads * kContribRowsPerThread;
+// Workgroups of the contrib launch over n_rows rows of the composed-LSE
+// array (the workspace holds one partial sum per workgroup and partition).
+int64_t contrib_blocks(int64_t n_rows);
 
 // bf16 inputs; states in bf16, or in float32 when state_f32
 hipError_t launch_attn_bf16(const AttnArgs& a, int D, bool state_f32, hipStream_t s);

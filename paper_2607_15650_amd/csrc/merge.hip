@@ -154,6 +154,9 @@ hipError_t launch_merge_d(const MergeArgs& a, int D, hipStream_t s) {
 // with a butterfly over the wave (lane l adds lane l^k's value, so every lane
 // holds the same bits) and the waves' sums are added in wave order: one
 // barrier for all partitions, and bitwise the same result on every run.
+constexpr int kContribThreads = 256;
+constexpr int kContribRowsPerThread = 2;
+constexpr int kContribRowsPerBlock = kContribThreads * kContribRowsPerThread;
 constexpr int kContribWaves = kContribThreads / 64;
 
 __device__ __forceinline__ float wave_sum(float x) {
@@ -164,27 +167,39 @@ __device__ __forceinline__ float wave_sum(float x) {
 
 template <int PMAX>
 __global__ __launch_bounds__(kContribThreads) void contrib_partial_kernel(const ContribArgs a) {
+  constexpr int R = kContribRowsPerThread;
   __shared__ float red[kContribWaves][PMAX];
   const int tid = threadIdx.x;
   const int P = a.P;
+  const int64_t n = a.n_rows;
+  const float* __restrict__ lse = a.lse;
+  const float* __restrict__ lse_out = a.lse_out;
+  float* __restrict__ w_rows = a.w_rows;
   const int64_t base = (int64_t)blockIdx.x * kContribRowsPerBlock;
+  // every load of the thread's rows first, then the weights: the loads are
+  // all in flight at once
+  float lo[R], lj[R][PMAX];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int64_t r = base + i * kContribThreads + tid;
+    const bool ok = r < n;
+    lo[i] = ok ? lse_out[r] : -INFINITY;
+#pragma unroll
+    for (int j = 0; j < PMAX; ++j) lj[i][j] = (ok && j < P) ? lse[(int64_t)j * n + r] : -INFINITY;
+  }
   float acc[PMAX];
 #pragma unroll
   for (int j = 0; j < PMAX; ++j) acc[j] = 0.f;
 #pragma unroll
-  for (int i = 0; i < kContribRowsPerThread; ++i) {
+  for (int i = 0; i < R; ++i) {
     const int64_t r = base + i * kContribThreads + tid;
-    if (r < a.n_rows) {
-      const float lo = a.lse_out[r];
 #pragma unroll
-      for (int j = 0; j < PMAX; ++j) {
-        if (j < P) {
-          const float lj = a.lse[(int64_t)j * a.n_rows + r];
-          float w = 0.f;
-          if (lo != -INFINITY && lj != -INFINITY) w = __builtin_amdgcn_exp2f((lj - lo) * kLog2e);
-          if (a.w_rows != nullptr) a.w_rows[r * P + j] = w;
-          acc[j] += w;
-        }
+    for (int j = 0; j < PMAX; ++j) {
+      if (j < P) {
+        float w = 0.f;
+        if (lo[i] != -INFINITY && lj[i][j] != -INFINITY) w = __builtin_amdgcn_exp2f((lj[i][j] - lo[i]) * kLog2e);
+        if (w_rows != nullptr && r < n) w_rows[r * P + j] = w;
+        acc[j] += w;
       }
     }
   }
@@ -205,15 +220,20 @@ __global__ __launch_bounds__(kContribThreads) void contrib_partial_kernel(const 
   }
 }
 
+// The workgroups' partial sums added in a fixed order by one wide workgroup
+// (its thread t takes partials t, t + kFinalThreads, ...).
+constexpr int kFinalThreads = 1024;
+constexpr int kFinalWaves = kFinalThreads / 64;
+
 template <int PMAX>
-__global__ __launch_bounds__(kContribThreads) void contrib_final_kernel(const ContribArgs a) {
-  __shared__ float red[kContribWaves][PMAX];
+__global__ __launch_bounds__(kFinalThreads) void contrib_final_kernel(const ContribArgs a) {
+  __shared__ float red[kFinalWaves][PMAX];
   const int tid = threadIdx.x;
   const int P = a.P;
   float acc[PMAX];
 #pragma unroll
   for (int j = 0; j < PMAX; ++j) acc[j] = 0.f;
-  for (int blk = tid; blk < a.n_blocks; blk += kContribThreads) {
+  for (int blk = tid; blk < a.n_blocks; blk += kFinalThreads) {
 #pragma unroll
     for (int j = 0; j < PMAX; ++j)
       if (j < P) acc[j] += a.partial[(int64_t)blk * P + j];
@@ -230,7 +250,7 @@ __global__ __launch_bounds__(kContribThreads) void contrib_final_kernel(const Co
   if (tid < P) {
     float sum = 0.f;
 #pragma unroll
-    for (int w = 0; w < kContribWaves; ++w) sum += red[w][tid];
+    for (int w = 0; w < kFinalWaves; ++w) sum += red[w][tid];
     a.w_part[tid] = a.n_rows > 0 ? sum / (float)a.n_rows : 0.f;
   }
 }
@@ -242,7 +262,7 @@ hipError_t launch_contrib_t(const ContribArgs& a, hipStream_t s) {
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(contrib_final_kernel<PMAX>, dim3(1), dim3(kContribThreads), 0, s, a);
+  hipLaunchKernelGGL(contrib_final_kernel<PMAX>, dim3(1), dim3(kFinalThreads), 0, s, a);
   return hipGetLastError();
 }
 
@@ -255,6 +275,8 @@ hipError_t launch_merge(const MergeArgs& a, ditango_dtype sdt, ditango_dtype odt
   if (sdt == DITANGO_F32 && odt == DITANGO_BF16) return launch_merge_d<float, __bf16>(a, D, s);
   return hipErrorInvalidValue;
 }
+
+int64_t contrib_blocks(int64_t n_rows) { return (n_rows + kContribRowsPerBlock - 1) / kContribRowsPerBlock; }
 
 hipError_t launch_contrib(const ContribArgs& a, hipStream_t s) {
   if (a.P <= 8) return launch_contrib_t<8>(a, s);

@@ -115,7 +115,7 @@ def test_contrib_argument_validation(L):
 
 def test_contrib_workspace_size(L):
     f = L.ditango_contrib_workspace_bytes
-    assert f(1, 40, 9450, 8) == ((40 * 9450 + 2047) // 2048) * 8 * 4
+    assert f(1, 40, 9450, 8) == ((40 * 9450 + 511) // 512) * 8 * 4
     assert f(0, 1, 1, 1) == 0
     assert f(1, 1, 1, 1) == 4
 
