@@ -157,51 +157,87 @@ __device__ __forceinline__ void store4(__bf16* p, const f32x4& x) {
 }
 __device__ __forceinline__ void store4(float* p, const f32x4& x) { *(f32x4*)p = x; }
 
-// Claims one unit of work from the queue counters for a workgroup past the
-// static ones (called by all 64 lanes of its first wave; the result is
-// wave-uniform).  Units: a main task id, or n_main + u for split unit u.
-// Order: this XCD's own queue; then, from one look at all the counters, the
-// main queue with the most units left, else the split queue; finally every
-// queue in turn.  Counters only grow, so a queue seen exhausted stays so, and
-// -1 (nothing left) is returned only after every queue was seen exhausted.
+// Work units of a launch: the main tasks [0, n_main), then the split units
+// n_main + u, u in [0, n_split * split_f) (split task n_main + u / split_f,
+// key range u % split_f).  XCD list x holds the x-th contiguous eighth of
+// the main tasks, then the x-th eighth of the split units; its first
+// n_static / 8 positions run static (workgroup b: position b / 8 of list
+// b % 8).  The rest of list x is claimed through two counters: queue x for
+// its main tasks, queue 8 + x for its split units.
+__device__ __forceinline__ int list_unit(const AttnArgs& a, int x, int t) {
+  const int lm = xcd_len(x, a.n_main);
+  return t < lm ? xcd_first(x, a.n_main) + t : a.n_main + xcd_first(x, a.n_split * a.split_f) + (t - lm);
+}
+// first list position and length handed out by queue q (0..15)
+__device__ __forceinline__ void queue_range(const AttnArgs& a, int q, int* first, int* len) {
+  const int x = q & 7;
+  const int s = a.n_static >> 3;
+  const int lm = xcd_len(x, a.n_main);
+  if (q < 8) {
+    *first = min(s, lm);
+    *len = lm - *first;
+  } else {
+    *first = max(s, lm);
+    *len = lm + xcd_len(x, a.n_split * a.split_f) - *first;
+  }
+}
+
+// Claims one unit for a workgroup past the static ones (called by all 64
+// lanes of its first wave; the result is wave-uniform).  Main tasks go
+// before split units, so that no short unit runs while a full task waits:
+// this XCD's main queue; then, from one look at all the counters, the main
+// queue with the most left; then this XCD's split queue, then the split
+// queue with the most left; finally every queue in turn.  Counters only
+// grow, so a queue seen exhausted stays so, and -1 (nothing left) is
+// returned only after every queue was seen exhausted.
 __device__ int claim_unit(const AttnArgs& a, int lane) {
   unsigned xcc;
   asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
   const int own = (int)(xcc & 7);
-  const int s = a.n_static >> 3;
-  const int n_tail = a.n_split * a.split_f;
-  auto qlen = [&](int q) { return q < 8 ? xcd_len(q, a.n_main) - s : (q == 8 ? n_tail : 0); };
   // one atomic increment of queue q (wave-uniform) by lane 0
   auto take = [&](int q) -> int {
-    const int len = qlen(q);
+    int first, len;
+    queue_range(a, q, &first, &len);
     if (len <= 0) return -1;
     int t = 0;
     if (lane == 0) t = __hip_atomic_fetch_add(a.queue + q, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     t = __builtin_amdgcn_readfirstlane(t);
-    if (t >= len) return -1;
-    return q < 8 ? xcd_first(q, a.n_main) + s + t : a.n_main + t;
+    return t < len ? list_unit(a, q & 7, first + t) : -1;
   };
   int u = take(own);
   if (u >= 0) return u;
+  bool own_split_tried = false;
   for (int it = 0; it < 4; ++it) {
     int left = 0;
-    if (lane < 9) left = qlen(lane) - __hip_atomic_load(a.queue + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    // main queue with the most left: max over lanes 0..7 of (left, lane)
-    int key = (lane < 8 && left > 0) ? (left << 3) | lane : -1;
+    if (lane < 16) {
+      int first, len;
+      queue_range(a, lane, &first, &len);
+      left = len - __hip_atomic_load(a.queue + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // the queue with the most left among lanes 0..7 (main), else among
+    // lanes 8..15 (split): max of (left, lane) within each group of 8
+    int key = left > 0 ? (left << 4) | lane : -1;
     key = max(key, __shfl_xor(key, 1));
     key = max(key, __shfl_xor(key, 2));
     key = max(key, __shfl_xor(key, 4));
-    key = __builtin_amdgcn_readfirstlane(key);
-    const int tail_left = __builtin_amdgcn_readlane(left, 8);
+    const int main_key = __builtin_amdgcn_readlane(key, 0);
+    const int split_key = __builtin_amdgcn_readlane(key, 8);
     int q;
-    if (key >= 0) q = key & 7;
-    else if (tail_left > 0) q = 8;
-    else return -1;
+    if (main_key >= 0) {
+      q = main_key & 15;
+    } else if (!own_split_tried && __builtin_amdgcn_readlane(left, 8 + own) > 0) {
+      q = 8 + own;
+      own_split_tried = true;
+    } else if (split_key >= 0) {
+      q = split_key & 15;
+    } else {
+      return -1;
+    }
     u = take(q);
     if (u >= 0) return u;
   }
-  for (int k = 1; k <= 8; ++k) {
-    u = take(k < 8 ? (own + k) & 7 : 8);
+  for (int k = 1; k < 16; ++k) {
+    u = take(k < 8 ? (own + k) & 7 : 8 + ((own + k) & 7));
     if (u >= 0) return u;
   }
   return -1;
@@ -215,24 +251,23 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
 
   // ---- task decode: (selected partition, batch, head, query tile), and for
   // a task of the split tail, which of its split_f key ranges
-  int task, part = -1;
+  int u;
   if ((int)blockIdx.x < a.n_static) {
-    task = xcd_first((int)blockIdx.x & 7, a.n_main) + ((int)blockIdx.x >> 3);
+    u = list_unit(a, (int)blockIdx.x & 7, (int)blockIdx.x >> 3);
   } else {
     int* claimed = (int*)(smem + 2 * NBUF * C::TILEB);
     if (threadIdx.x < 64) {
-      const int u = claim_unit(a, (int)threadIdx.x);
-      if (threadIdx.x == 0) *claimed = u;
+      const int c = claim_unit(a, (int)threadIdx.x);
+      if (threadIdx.x == 0) *claimed = c;
     }
     __syncthreads();
-    const int u = __builtin_amdgcn_readfirstlane(*claimed);
+    u = __builtin_amdgcn_readfirstlane(*claimed);
     if (u < 0) return;
-    if (u < a.n_main) {
-      task = u;
-    } else {
-      task = a.n_main + (u - a.n_main) / a.split_f;
-      part = (u - a.n_main) % a.split_f;
-    }
+  }
+  int task = u, part = -1;
+  if (u >= a.n_main) {
+    task = a.n_main + (u - a.n_main) / a.split_f;
+    part = (u - a.n_main) % a.split_f;
   }
   const int qt = task % a.q_tiles;
   int t = task / a.q_tiles;
@@ -699,7 +734,9 @@ hipError_t plan_cfg(const AttnArgs& a, Plan* p) {
   if (e != hipSuccess) return e;
   p->slots = (int64_t)cus * (occ > 0 ? occ : 1);
   p->bytes = kQueueBytes;
-  const int f = plan_tail_split(nblk, p->slots);
+  // the split tasks are the launch's last ones: tiles of the last selected partition
+  const int64_t tiles = ((int64_t)a.kv_len[a.n_sel - 1] + BN - 1) / BN;
+  const int f = plan_tail_split(nblk, p->slots, tiles);
   if (f <= 1) return hipSuccess;
   p->f = f;
   p->n_split = nblk % p->slots;
@@ -742,16 +779,30 @@ hipError_t launch_cfg(const AttnArgs& a0, void* ws, size_t ws_bytes, hipStream_t
       a.part_out = (float*)((char*)ws + kQueueBytes);
       a.part_lse = (float*)((char*)a.part_out + align256((size_t)p.n_split * p.f * C::BM * D * sizeof(float)));
     }
-    // static share: all but the last DITANGO_DYN_ROUNDS rounds of every
-    // XCD's range; one extra round of workgroups lets the faster XCDs take
-    // units from the slower ones' queues
-    const int64_t per_xcd_slots = p.slots / 8 > 0 ? p.slots / 8 : 1;
-    const int64_t st = (int64_t)(a.n_main / 8) - DITANGO_DYN_ROUNDS * per_xcd_slots;
-    a.n_static = st > 0 ? (int)(8 * st) : 0;
-    grid = (int64_t)a.n_main + (int64_t)a.n_split * a.split_f + 8 * per_xcd_slots;
-    hipLaunchKernelGGL(attn_queue_reset_kernel, dim3(1), dim3(64), 0, s, a.queue);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    // static share: the first positions of every XCD queue, all but its
+    // last DITANGO_DYN_ROUNDS rounds and at least the first round (which
+    // starts at once and gains nothing from claiming); as many extra
+    // workgroups as dynamic units, up to one round, let the faster XCDs
+    // take units from the slower ones' queues
+    const int64_t per_xcd = p.slots / 8 > 0 ? p.slots / 8 : 1;
+    const int64_t n_tail = (int64_t)a.n_split * a.split_f;
+    int64_t min_len = INT64_MAX;
+    for (int x = 0; x < 8; ++x) {
+      const int64_t len = (a.n_main >> 3) + (x < (a.n_main & 7) ? 1 : 0) + (n_tail >> 3) + (x < (n_tail & 7) ? 1 : 0);
+      min_len = len < min_len ? len : min_len;
+    }
+    int64_t st = min_len - DITANGO_DYN_ROUNDS * per_xcd;
+    const int64_t first = min_len < per_xcd ? min_len : per_xcd;
+    st = st > first ? st : first;
+    const int64_t n_units = (int64_t)a.n_main + n_tail;
+    const int64_t n_dyn = n_units - 8 * st;
+    a.n_static = (int)(8 * st);
+    grid = n_units + (n_dyn < p.slots ? n_dyn : p.slots);
+    if (n_dyn > 0) {
+      hipLaunchKernelGGL(attn_queue_reset_kernel, dim3(1), dim3(64), 0, s, a.queue);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
   }
   hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>), dim3((unsigned)grid), dim3(C::NT), lds,
                      s, a);

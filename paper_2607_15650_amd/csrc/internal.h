@@ -37,15 +37,16 @@ struct AttnArgs {
   int split_f;
   float* part_out;          // [n_split * split_f][rows per workgroup][D]
   float* part_lse;          // [n_split * split_f][rows per workgroup]
-  // Balancing over the XCDs (bf16 kernel, with a workspace).  The main tasks
-  // are cut into 8 contiguous ranges, one per XCD (xcd_first / xcd_len).
-  // Workgroups [0, n_static) run fixed tasks: workgroup b the (b / 8)-th
-  // task of range b % 8.  Every later workgroup claims one unit from the
-  // queue counters: queue x < 8 holds the rest of range x, queue 8 the
-  // n_split * split_f split units; its own XCD's queue first, then the main
-  // queue with the most left, then the split queue; it exits when all are
-  // exhausted.  queue = null: no queues, every workgroup is static
-  // (n_static = n_main).
+  // Balancing over the XCDs (bf16 kernel, with a workspace).  The units of
+  // work (main tasks, then split units) are dealt into 8 lists, one per
+  // XCD: list x holds the x-th contiguous eighth of the main tasks, then the
+  // x-th eighth of the split units.  Workgroups [0, n_static) run fixed
+  // units: workgroup b position b / 8 of list b % 8.  Every later workgroup
+  // claims one unit from the queue counters of the positions past
+  // n_static / 8 (queue x: list x's main tasks, queue 8 + x: its split
+  // units): main tasks anywhere before split units, its own XCD's first; it
+  // exits when all are exhausted.  queue = null: no queues, every workgroup
+  // is static (n_static = n_main, no split units).
   int n_static;
   int* queue;               // kQueueInts counters, zeroed before the launch
 };
@@ -54,25 +55,44 @@ constexpr int kMaxSplit = 8;
 constexpr int kQueueInts = 16;
 constexpr size_t kQueueBytes = 256;   // the queue counters, at the start of the workspace
 
-// Tail split plan: with `slots` workgroups resident at once and `tasks`
-// equal-length tasks, the last round runs tasks % slots of them; splitting
-// each of those into f key ranges shortens it to ceil(f * rem / slots) / f
-// of a task.  Returns the f in [2, kMaxSplit] that minimises that (the
-// smallest on ties), or 1 when no split shortens the last round.
-inline int plan_tail_split(int64_t tasks, int64_t slots) {
-  if (slots <= 0) return 1;
+// Tail split plan.  With `slots` workgroups resident at once and `tasks`
+// tasks of `tiles` key tiles each, the last round runs rem = tasks % slots
+// of them.  Its cost, in key tiles, is estimated as tiles + kMainUnitCost
+// unsplit; split into f key ranges it is ceil(f * rem / slots) rounds of
+// ceil(tiles / f) + kSplitUnitCost (a split unit loads its queries again and
+// writes its partial state in float32), plus kFixupCost for the kernel that
+// composes the partials.  Returns the f in [2, kMaxSplit] with the lowest
+// estimate (the smallest on ties) when it is at least 3 % below the
+// unsplit one, else 1.  Launches with more than kMaxSplitRounds full rounds
+// before the last are not split: the workgroups' speeds differ by a few
+// percent, so after many rounds their finish times are spread over much of
+// a task and the queue counters hand the last tasks to the earliest
+// finishers (measured: a 4,440-task launch on 256 CUs ran 0.4-1.2 % faster
+// balanced and unsplit than balanced and split 5 or 8 ways, on three
+// cards; 1,480 and 8,880 tasks alike; a 216-task single round of 22-tile
+// tasks was twice as slow split 7 ways).
+constexpr int kMainUnitCost = 1;
+constexpr int kSplitUnitCost = 4;
+constexpr int kFixupCost = 3;
+constexpr int kMaxSplitRounds = 4;
+
+inline int plan_tail_split(int64_t tasks, int64_t slots, int64_t tiles) {
+  if (slots <= 0 || tiles <= 0) return 1;
+  if (tasks / slots > kMaxSplitRounds) return 1;
   const int64_t rem = tasks % slots;
   if (rem == 0) return 1;
+  const double unsplit = (double)(tiles + kMainUnitCost);
   int best = 1;
-  double best_t = 1.0;
+  double best_t = unsplit;
   for (int f = 2; f <= kMaxSplit; ++f) {
-    const double t = (double)((f * rem + slots - 1) / slots) / f;
-    if (t < best_t - 1e-12) {
+    const int64_t rounds = (f * rem + slots - 1) / slots;
+    const double t = (double)(rounds * ((tiles + f - 1) / f + kSplitUnitCost) + kFixupCost);
+    if (t < best_t - 1e-9) {
       best_t = t;
       best = f;
     }
   }
-  return best;
+  return best_t <= 0.97 * unsplit ? best : 1;
 }
 
 struct MergeArgs {

@@ -43,8 +43,9 @@ def run_step(w, x, select, rows_prev=True):
     if "q_prev" in dev:
         a.attn_partition_states(dev["q_prev"][:, qa:qb].contiguous(), dev["k_prev"], dev["v_prev"],
                                 offs, [1] * P, w.scale, out_states, lse_states)
-    # the current step as bench.py launches it: with the workspace that splits
-    # the launch's last round when that shortens it
+    # the current step as bench.py launches it: with the workspace whose
+    # queue counters balance the launch over the XCDs (and that splits the
+    # last round of a launch of few rounds)
     mask = [1 if j in select else 0 for j in range(P)]
     n_ws = a.attn_workspace_bytes(torch_dtype(w.dtype), w.B, w.H, w.D, q_len, offs, mask)
     ws_attn = torch.empty(n_ws, dtype=torch.uint8, device="cuda") if n_ws > 0 else None

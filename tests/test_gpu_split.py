@@ -4,9 +4,8 @@ composed by a fix-up kernel.  Checked against the float64 oracle, against
 the unsplit launch, for determinism, and for leaving unselected slots alone.
 
 Shapes are chosen from the device's compute-unit count so that one full
-round plus 16 tasks is launched: the 16 tail tasks are split 8 ways, and
-the key ranges include partial tiles and, for the long partition, an empty
-range.
+round plus 16 tasks is launched: the 16 tail tasks are split 7 or 8 ways,
+and the last key range of each ends in a partial tile.
 """
 import numpy as np
 import pytest
@@ -27,7 +26,7 @@ def api():
 # (D, partition lengths, selected partitions, state dtype): the last
 # selected partition owns the split tail tasks
 CASES = [
-    (128, [500, 2081, 90], (0, 1), "bf16"),     # long tail partition: 33 tiles, range 7 of 8 empty
+    (128, [500, 2081, 90], (0, 1), "bf16"),     # long tail partition: 33 tiles, 7 ranges of 5 (the last 3)
     (128, [2081, 500, 90], (0, 1), "bf16"),     # short tail partition: 8 tiles, one per range
     (64, [700, 1234, 33], (0, 1), "bf16"),
     (128, [300, 1000, 0], (0, 1), "f32"),       # float32 states for bf16 inputs
@@ -104,6 +103,20 @@ def test_tail_split_matches_oracle_and_unsplit(D, lens, select, state_dt):
         # round differently (OUT), and the composition adds its own (LSE)
         assert max_abs(g_lse, l_plain[j].cpu().numpy()) <= 1e-4
         assert max_abs(g_out, s_plain[j].float().cpu().numpy()) <= tol["out"]
+
+
+def test_no_split_of_short_tasks_in_a_single_round():
+    """216 tasks of 22 key tiles on 256 compute units: splitting them would
+    make units of 3-4 tiles whose fixed costs (queries loaded again, float32
+    partial states written and composed) outweigh the shorter round."""
+    import torch
+    a = api()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    if cus <= 216:
+        pytest.skip("needs more than 216 compute units")
+    offs = [2048 * j for j in range(9)]
+    sel = [0, 0, 1, 1, 1, 0, 0, 0]
+    assert a.attn_workspace_bytes(torch.bfloat16, 1, 12, 64, 2048, offs, sel) == 256
 
 
 def test_no_split_when_the_last_round_is_full():
