@@ -246,8 +246,12 @@ __device__ int claim_unit(const AttnArgs& a, int lane) {
 template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
 __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs a) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
-  // 2*NBUF tiles, then one int: the claimed unit of a queue workgroup
+  // LDS: the K and V rings (2*NBUF tiles), then one staging region per wave
+  // (its QB*32 rows of Q on the way in, of OUT on the way out), then one
+  // int: the claimed unit of a queue workgroup
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+  constexpr int kStage = 2 * NBUF * C::TILEB;
+  constexpr int kStageWave = QB * 32 * C::ROWB;
 
   // ---- task decode: (selected partition, batch, head, query tile), and for
   // a task of the split tail, which of its split_f key ranges
@@ -255,7 +259,7 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   if ((int)blockIdx.x < a.n_static) {
     u = list_unit(a, (int)blockIdx.x & 7, (int)blockIdx.x >> 3);
   } else {
-    int* claimed = (int*)(smem + 2 * NBUF * C::TILEB);
+    int* claimed = (int*)(smem + kStage + NW * kStageWave);
     if (threadIdx.x < 64) {
       const int c = claim_unit(a, (int)threadIdx.x);
       if (threadIdx.x == 0) *claimed = c;
@@ -299,21 +303,24 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   const __bf16* __restrict__ kg = (const __bf16*)a.k + ((int64_t)b * a.S + kv0) * HD + (int64_t)h * D;
   const __bf16* __restrict__ vg = (const __bf16*)a.v + ((int64_t)b * a.S + kv0) * HD + (int64_t)h * D;
 
-  // ---- Q^T fragments (B operand): lane holds Q[row][16s + 8g .. +8]
+  // ---- Q^T fragments (B operand): lane holds Q[row][16s + 8g .. +8].  The
+  // wave's QB*32 query rows come in through its LDS staging region, loaded
+  // like a K tile (whole rows per 1 KiB load, units swizzled by row), and are
+  // read back once the loads have landed (unstage_q).
   const int64_t row0 = (int64_t)qt * C::BM + wave * (QB * 32);
   bf16x8 qf[QB][C::KS];
+  const unsigned char* stage = smem + kStage + wave * kStageWave;
+  // 16-byte unit swizzle of an OUT row staged for the store: consecutive
+  // rows of one accumulator register land in distinct bank groups
+  auto swz_out = [](int row) { return row & (C::UNITS - 1); };
+  auto unstage_q = [&]() {
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int64_t row = row0 + qb * 32 + lr;
-    if (row < a.q_len) {
-      const __bf16* src = qg + ((int64_t)b * a.q_len + row) * HD + (int64_t)h * D + 8 * g;
+    for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-      for (int s = 0; s < C::KS; ++s) qf[qb][s] = *(const bf16x8*)(src + 16 * s);
-    } else {
-#pragma unroll
-      for (int s = 0; s < C::KS; ++s) qf[qb][s] = bf16x8{};
-    }
-  }
+      for (int s = 0; s < C::KS; ++s)
+        qf[qb][s] = *(const bf16x8*)(stage + (qb * 32 + lr) * C::ROWB +
+                                     (((2 * s + g) ^ swz_k<D>(qb * 32 + lr)) * 16));
+  };
 
   f32x16 o[QB][C::DB];
   float m[QB], l[QB];
@@ -345,6 +352,18 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
     ld_off_v[i] = row * row_bytes + (uint32_t)((ld_unit ^ swz_v<D>(row)) * 16);
   }
   const uint32_t smem_lds = lds_addr(smem);
+  if (kv_len > 0) {
+    // rows past q_len are clamped to the last row: computed, never stored
+    const int64_t rb0 = min(row0, a.q_len - 1);
+    const __bf16* base = qg + ((int64_t)b * a.q_len + rb0) * HD + (int64_t)h * D;
+    const uint32_t dst = smem_lds + (uint32_t)(kStage + wave * kStageWave);
+#pragma unroll
+    for (int i = 0; i < kStageWave / 1024; ++i) {
+      const int row = i * C::ROWS_PER_LOAD + ld_row;
+      const int64_t gr = min(row0 + row, a.q_len - 1) - rb0;
+      lds_dma16(base, (uint32_t)gr * row_bytes + (uint32_t)((ld_unit ^ swz_k<D>(row)) * 16), dst + (uint32_t)(i * 1024));
+    }
+  }
   auto load_tile = [&](const __bf16* src, uint32_t dst, int key0, bool is_k) {
     if (key0 + BN <= kv_len) {
       const __bf16* base = src + (int64_t)key0 * HD;
@@ -542,7 +561,8 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
         load_tile(kg, kbuf_lds(j), j * BN, true);
         load_tile(vg, vbuf_lds(j), j * BN, false);
       }
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // tile 0 has landed
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // the queries and tile 0 have landed
+      unstage_q();
       __syncthreads();
       for (int i = 0; i < n_tiles; ++i) {
         // tile i+PF replaces tile i+PF-NBUF, consumed before the last barrier
@@ -569,7 +589,8 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
         load_tile(kg, kbuf_lds(j + 1 + C::PF), (j + 1 + C::PF) * BN, true);
         load_tile(vg, vbuf_lds(j + C::PF), (j + C::PF) * BN, false);
       }
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // K_0, K_1, V_0 have landed
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(C::VM_LEFT));   // the queries, K_0, K_1, V_0 have landed
+      unstage_q();
       __syncthreads();
       qk(kbuf(0), s0);
       // every wave has read K_0 before iteration 0 loads K_2 into its slot
@@ -595,17 +616,33 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
       const float inv = lt > 0.f ? 1.0f / lt : 0.f;
       const float lse = lt > 0.f ? (m[qb] + __builtin_amdgcn_logf(lt)) * kLn2 : -INFINITY;
       if (part < 0) {
-        TS* dst = outg + (int64_t)slot * slot_elems + ((int64_t)b * a.q_len + row) * HD +
-                      (int64_t)h * D + 4 * g;
+        if constexpr (sizeof(TS) == 2 && D == 128) {
+          // bf16 states: into the wave's staging region (row-major, 16-byte
+          // units swizzled by row), stored below as whole rows
+          unsigned char* srow = (unsigned char*)stage + (qb * 32 + lr) * C::ROWB;
 #pragma unroll
-        for (int db = 0; db < C::DB; ++db)
+          for (int db = 0; db < C::DB; ++db)
 #pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4) {
-            f32x4 x;
+            for (int r4 = 0; r4 < 4; ++r4) {
+              f32x4 x;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
-            store4(dst + db * 32 + 8 * r4, x);
-          }
+              for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
+              const int unit = (4 * db + r4) ^ swz_out(qb * 32 + lr);
+              *(bf16x4*)(srow + unit * 16 + 8 * g) = __builtin_convertvector(x, bf16x4);
+            }
+        } else {
+          TS* dst = outg + (int64_t)slot * slot_elems + ((int64_t)b * a.q_len + row) * HD +
+                        (int64_t)h * D + 4 * g;
+#pragma unroll
+          for (int db = 0; db < C::DB; ++db)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+              f32x4 x;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
+              store4(dst + db * 32 + 8 * r4, x);
+            }
+        }
         if (g == 0) a.lse_states[(((int64_t)slot * a.B + b) * a.H + h) * a.q_len + row] = lse;
       } else {
         const int64_t rl = row - (int64_t)qt * C::BM;            // row within the query tile
@@ -620,6 +657,22 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
             store4(dst + db * 32 + 8 * r4, x);
           }
         if (g == 0) a.part_lse[pt * C::BM + rl] = lse;
+      }
+    }
+  }
+  if constexpr (sizeof(TS) == 2 && D == 128) {
+    if (part < 0) {
+      // the staged rows, whole: lane l stores unit l % UNITS of row
+      // l / UNITS + ROWS_PER_LOAD * i (the wave's own region, so its LDS
+      // writes above are visible to these reads without a barrier)
+      TS* dst0 = outg + (int64_t)slot * slot_elems + (int64_t)b * a.q_len * HD + (int64_t)h * D + ld_unit * 8;
+#pragma unroll
+      for (int i = 0; i < QB * 32 / C::ROWS_PER_LOAD; ++i) {
+        const int row = i * C::ROWS_PER_LOAD + ld_row;
+        if (row0 + row < a.q_len) {
+          const bf16x8 x = *(const bf16x8*)(stage + row * C::ROWB + ((ld_unit ^ swz_out(row)) * 16));
+          *(bf16x8*)(dst0 + (row0 + row) * HD) = x;
+        }
       }
     }
   }
@@ -719,7 +772,7 @@ hipError_t set_lds(size_t lds) {
 template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
 hipError_t plan_cfg(const AttnArgs& a, Plan* p) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
-  const size_t lds = (size_t)2 * NBUF * C::TILEB + 16;
+  const size_t lds = (size_t)2 * NBUF * C::TILEB + (size_t)NW * QB * 32 * C::ROWB + 16;
   hipError_t e = set_lds<D, QB, NW, BN, NBUF, WPE, SEQ, TS>(lds);
   if (e != hipSuccess) return e;
   *p = Plan{};
@@ -749,7 +802,7 @@ hipError_t plan_cfg(const AttnArgs& a, Plan* p) {
 template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
 hipError_t launch_cfg(const AttnArgs& a0, void* ws, size_t ws_bytes, hipStream_t s) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
-  const size_t lds = (size_t)2 * NBUF * C::TILEB + 16;
+  const size_t lds = (size_t)2 * NBUF * C::TILEB + (size_t)NW * QB * 32 * C::ROWB + 16;
   Plan p;
   const bool queued = ws != nullptr && ws_bytes >= kQueueBytes;
   if (queued) {
