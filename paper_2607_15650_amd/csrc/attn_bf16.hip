@@ -310,8 +310,9 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   const int64_t row0 = (int64_t)qt * C::BM + wave * (QB * 32);
   bf16x8 qf[QB][C::KS];
   const unsigned char* stage = smem + kStage + wave * kStageWave;
-  // 16-byte unit swizzle of an OUT row staged for the store: consecutive
-  // rows of one accumulator register land in distinct bank groups
+  // 16-byte unit swizzle of an OUT row staged for the store: rows r..r+15
+  // of one accumulator register land in distinct bank groups (rows r and
+  // r + 16 also swap the two 8-byte halves of a unit)
   auto swz_out = [](int row) { return row & (C::UNITS - 1); };
   auto unstage_q = [&]() {
 #pragma unroll
@@ -627,8 +628,10 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
               f32x4 x;
 #pragma unroll
               for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
+              // rows r and r + 16 share a unit, so they take opposite halves
               const int unit = (4 * db + r4) ^ swz_out(qb * 32 + lr);
-              *(bf16x4*)(srow + unit * 16 + 8 * g) = __builtin_convertvector(x, bf16x4);
+              const int half = g ^ ((lr >> 4) & 1);
+              *(bf16x4*)(srow + unit * 16 + 8 * half) = __builtin_convertvector(x, bf16x4);
             }
         } else {
           TS* dst = outg + (int64_t)slot * slot_elems + ((int64_t)b * a.q_len + row) * HD +
@@ -670,7 +673,8 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
       for (int i = 0; i < QB * 32 / C::ROWS_PER_LOAD; ++i) {
         const int row = i * C::ROWS_PER_LOAD + ld_row;
         if (row0 + row < a.q_len) {
-          const bf16x8 x = *(const bf16x8*)(stage + row * C::ROWB + ((ld_unit ^ swz_out(row)) * 16));
+          bf16x8 x = *(const bf16x8*)(stage + row * C::ROWB + ((ld_unit ^ swz_out(row)) * 16));
+          if ((row >> 4) & 1) x = __builtin_shufflevector(x, x, 4, 5, 6, 7, 0, 1, 2, 3);
           *(bf16x8*)(dst0 + (row0 + row) * HD) = x;
         }
       }
