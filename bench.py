@@ -66,6 +66,9 @@ def parse():
     ap.add_argument("--attn-workspace", choices=("full", "queue", "none"), default="full",
                     help="workspace of the attention launch: queue counters and tail-split partials (full), "
                          "the queue counters only (balanced, unsplit), or none (static launch)")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the step as one captured HIP graph (counter reset, attention, merge, weights) "
+                         "replayed --steps times; the per-kernel times stay eager")
     ap.add_argument("--no-selection-sweep", dest="selection_sweep", action="store_false",
                     help="skip the step-time-against-selected-fraction points")
     ap.add_argument("--power-seconds", type=float, default=3.0,
@@ -554,13 +557,23 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] workload {w.name} select {list(select)} warmup {args.warmup} done", file=sys.stderr, flush=True)
 
-    # pass 1: whole-step wall clock (events only at the ends)
+    # pass 1: whole-step wall clock (events only at the ends); with --graph
+    # the step is captured once and replayed
+    run_step = step
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        run_step = graph.replay
+        for _ in range(max(1, args.warmup)):
+            run_step()
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
     for _ in range(args.steps):
-        step()
+        run_step()
     stop.record()
     torch.cuda.synchronize()
     ms_per_step = start.elapsed_time(stop) / args.steps
@@ -678,7 +691,7 @@ def main():
         "config": {"workload": w.name, "B": w.B, "H": w.H, "D": w.D, "S": w.S, "P": w.P,
                    "query_partition": w.q, "q_len": q_len, "fresh_partitions": list(select),
                    "fresh_fraction": len(select) / w.P,
-                   "attn_launch": attn_mode(ws_attn),
+                   "attn_launch": attn_mode(ws_attn), "step_graph": bool(args.graph),
                    "attn_workspace_bytes": int(ws_attn.numel()) if ws_attn is not None else 0},
         "roofline": {"bound": "mfma",
                      "kernel": attn_kernels(ws_attn) if w.dtype == "bf16" else "attn_f32_kernel",
