@@ -241,6 +241,24 @@ def test_ragged_shapes(dtype, D, H, q_len, lens):
     mo, ml = oracle.merge(outs, lses)
     assert max_abs(out.float().cpu().numpy(), mo) <= tol["out"]
     assert max_abs(lse.cpu().numpy(), ml) <= tol["lse"]
+    # the same launch with the attention workspace (queue counters, and a
+    # split last round when the plan asks for one): bit for bit the static
+    # launch when unsplit, within the tolerance of the oracle when split
+    need = a.attn_workspace_bytes(torch_dtype(dtype), B, H, D, q_len, offs, [1] * P)
+    if need > 0:
+        ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        ws.fill_(0x5A)                                  # stale counters
+        s2, l2 = new_state_cache(P, B, q_len, H, D, dtype)
+        a.attn_partition_states(to_gpu(q, dtype), to_gpu(k, dtype), to_gpu(v, dtype), offs, [1] * P, scale,
+                                s2, l2, ws)
+        torch.cuda.synchronize()
+        if need == 256:
+            assert torch.equal(s2.view(torch.uint8), out_states.view(torch.uint8))
+            assert torch.equal(l2.view(torch.int32), lse_states.view(torch.int32))
+        else:
+            for j in range(P):
+                assert max_abs(s2[j].float().cpu().numpy(), outs[j]) <= tol["out"], j
+                assert max_abs(l2[j].cpu().numpy(), lses[j]) <= tol["lse"], j
 
 
 @pytest.mark.parametrize("D", [128, 64])
