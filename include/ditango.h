@@ -109,12 +109,16 @@ ditango_status ditango_attn_partition_states_ex(
  * A launch is a set of tasks (query tile x head x batch x selected
  * partition) of which the GPU runs a fixed number at a time.
  *  - Balancing: the first 256 bytes of the workspace hold queue counters
- *    (zeroed by a small kernel on `stream` before the launch).  Most tasks
- *    run where the hardware places them; the last ones are claimed from the
- *    counters, so that XCDs that run faster take more of them.
- *  - Tail split: when the last round is partly filled, its tasks are split
- *    into up to 8 key ranges whose partial states go to the rest of the
- *    workspace and are composed into their slots by a second small kernel.
+ *    (zeroed by a small kernel on `stream` before a launch that claims any
+ *    task).  Most tasks run where the hardware places them; the last ones
+ *    are claimed from the counters, so that XCDs that run faster take more
+ *    of them.
+ *  - Tail split: when the last round is partly filled, the launch has at
+ *    most 4 full rounds before it (after more, balancing evens out its
+ *    end) and an estimate of the round's cost in key tiles says a split
+ *    saves 3 %, its tasks are split into up to 8 key ranges whose partial
+ *    states go to the rest of the workspace and are composed into their
+ *    slots by a second small kernel.
  *
  *   workspace        device, 256-byte aligned.  NULL or under 256 bytes:
  *                    the static launch of ditango_attn_partition_states_ex;
