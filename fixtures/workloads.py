@@ -11,8 +11,10 @@ the paper; partition adjacency follows Fig. 2).
 Shapes follow the paper's video-DiT workloads (Table 1 of Sec. 6.1): the
 75,600-token, 40-head, head-dim-128 case is Wan2.1-14B's 81-frame 720p latent;
 the 131,072-token case stands for the long-context HunyuanVideo-scale sequence.
-Batch is 1 everywhere (the paper's classifier-free-guidance batch of 2 is a
-second workload variant that is not built here).
+Batch is 1 in the five main workloads; the paper's classifier-free-guidance
+batch of 2 (the conditional and unconditional branch of one denoising step)
+is the separate ``videodit_cfg_bf16_b2_h40_d128_s75600_p8`` variant below,
+beside the HunyuanVideo-like head-dim-64 shape.
 """
 from __future__ import annotations
 

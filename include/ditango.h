@@ -74,7 +74,9 @@ typedef enum {
  *                (DITANGO_ERR_UNSUPPORTED beyond).
  *   kv_offsets   host, P+1 int64, kv_offsets[0] = 0, non-decreasing.
  *   select       host, P bytes; non-zero = compute partition j fresh.
- *   scale        softmax scale applied to q.k (normally 1/sqrt(D)).
+ *   scale        softmax scale applied to q.k (normally 1/sqrt(D)); finite
+ *                and > 0 (DITANGO_ERR_INVALID otherwise: zero, negative,
+ *                inf and NaN are rejected before anything is launched).
  *   out_states   device, [P][B][q_len][H][D] in dtype `dt`.
  *   lse_states   device, [P][B][H][q_len] float32.
  *

@@ -6,6 +6,11 @@ Eq. scale_ratio, Eq. error_extrapolation); anchors when every group exceeds
 eps or the relative local drift exceeds eps_local (Sec. 4.2.4); eps is the
 R-quantile of the anchor correction errors w(G) ||fresh(G) - cached(G)||,
 and before any exist the R-quantile of the current step's ASE values.
+
+Each step's result also records the step every group was last computed at
+(``t_c``) and every anchor correction error recorded so far
+(``corrections``, in the order they were recorded: anchor by anchor, groups
+in order).
 """
 from __future__ import annotations
 
@@ -23,7 +28,11 @@ def r_quantile(values, r):
     return v[max(0, min(len(v) - 1, int(math.ceil(r * len(v))) - 1))]
 
 
-def run(steps: Sequence[Dict[str, np.ndarray]], offsets, q, g, R, eps_local, scale):
+def run(steps: Sequence[Dict[str, np.ndarray]], offsets, q, g, R, eps_local, scale, force=None):
+    """``force`` (optional) maps a step t to a decision (anchor, groups to
+    compute) taken instead of the rule's, after the rule's inputs (ASE,
+    drift, eps) have been formed: a test re-synchronises with a run whose
+    decision differed on a near-tie."""
     P = len(offsets) - 1
     groups = groups_of(P, q, g)
     part = lambda qx, x, j: partition_state(qx, x["k"][:, offsets[j]:offsets[j + 1]],
@@ -46,6 +55,9 @@ def run(steps: Sequence[Dict[str, np.ndarray]], offsets, q, g, R, eps_local, sca
             if eps is None:
                 eps = r_quantile(list(ase.values()), R)
             anchor = all(ase[grp] > eps for grp in groups) or drift > eps_local
+        forced = force is not None and t in force
+        if forced:
+            anchor = bool(force[t][0])
         if anchor:
             compute = list(groups)
             sts = [part(qx, x, j) for j in range(P)]
@@ -67,6 +79,8 @@ def run(steps: Sequence[Dict[str, np.ndarray]], offsets, q, g, R, eps_local, sca
             snap = {t: local[0]}
         else:
             compute = [grp for grp in groups if ase[grp] > eps]
+            if forced:
+                compute = [tuple(grp) for grp in force[t][1]]
             for grp in compute:
                 sts = [part(qx, x, j) for j in range(*grp)]
                 cache[grp] = merge([s_[0] for s_ in sts], [s_[1] for s_ in sts])
@@ -75,5 +89,6 @@ def run(steps: Sequence[Dict[str, np.ndarray]], offsets, q, g, R, eps_local, sca
                 snap[t] = local[0]
         out, lse = merge([cache[grp][0] for grp in groups] + [local[0]],
                          [cache[grp][1] for grp in groups] + [local[1]])
-        results.append(dict(anchor=anchor, compute=compute, ase=ase, eps=eps, drift=drift, out=out, lse=lse))
+        results.append(dict(anchor=anchor, compute=compute, ase=ase, eps=eps, drift=drift, out=out, lse=lse,
+                            t_c=dict(t_c), corrections=list(corrections)))
     return results

@@ -18,10 +18,13 @@ from .state import contrib, merge, partition_state, plan_threshold
 
 
 def run(steps: Sequence[Dict[str, np.ndarray]], offsets: Sequence[int], blocks: Sequence[int],
-        anchors: Sequence[int], threshold: float, scale: float):
+        anchors: Sequence[int], threshold: float, scale: float, force=None):
     """``steps[s]`` holds float64 q, k, v [B, S, H, D] of step s.
 
     Returns a list over steps of dicts {block: (mask, out, lse, wbar)}.
+    ``force`` (optional) maps (step, block) to a mask used instead of the
+    rule's: a test re-synchronises with a run whose mask differed on a
+    near-tie.
     """
     P = len(offsets) - 1
     cache = {qb: [None] * P for qb in blocks}
@@ -34,6 +37,8 @@ def run(steps: Sequence[Dict[str, np.ndarray]], offsets: Sequence[int], blocks: 
                 mask = [1] * P
             else:
                 mask = plan_threshold(anchor_w[qb], qb, threshold)
+            if force is not None and (s, qb) in force:
+                mask = list(force[(s, qb)])
             q = x["q"][:, offsets[qb]:offsets[qb + 1]]
             for j in range(P):
                 if mask[j]:

@@ -27,6 +27,7 @@ from __future__ import annotations
 import math
 from typing import Dict, List, Optional, Sequence, Tuple
 
+import numpy as np
 import torch
 
 from . import api
@@ -35,10 +36,11 @@ from .groups import base_groups
 
 
 def quantile_r(values: Sequence[float], r: float) -> float:
-    """The value below or at which a fraction r of ``values`` lie: sorted[ceil(r*m) - 1]."""
-    v = sorted(float(x) for x in values)
-    i = max(0, min(len(v) - 1, int(math.ceil(r * len(v))) - 1))
-    return v[i]
+    """The smallest value with at least a fraction r of ``values`` at or below
+    it (the ceil(r*m)-th smallest of m values; the smallest for r <= 0)."""
+    v = np.sort(np.asarray(values, dtype=np.float64))
+    k = min(max(int(math.ceil(r * v.size)), 1), v.size)
+    return float(v[k - 1])
 
 
 class ErrorModelSelectiveAttention:

@@ -45,7 +45,9 @@ ditango_status attn_args(const void* q, const void* k, const void* v, ditango_dt
   if (B < 1 || H < 1 || q_len < 1 || P < 1) return DITANGO_ERR_INVALID;
   if (P > kMaxParts) return DITANGO_ERR_UNSUPPORTED;
   if (D != 64 && D != 128) return DITANGO_ERR_UNSUPPORTED;
-  if (!isfinite(scale)) return DITANGO_ERR_INVALID;
+  // the kernels mask keys past a partition's end to -inf before scaling and
+  // take the running maximum of the unscaled scores: both need scale > 0
+  if (!isfinite(scale) || !(scale > 0.f)) return DITANGO_ERR_INVALID;
   if (kv_offsets[0] != 0) return DITANGO_ERR_INVALID;
   for (int j = 0; j < P; ++j) {
     if (kv_offsets[j + 1] < kv_offsets[j]) return DITANGO_ERR_INVALID;

@@ -13,15 +13,23 @@ from __future__ import annotations
 
 from typing import Dict, List, Optional, Sequence
 
+import numpy as np
+
 
 def rank_partitions(wbar: Sequence[float], q: int) -> List[int]:
-    """Partitions by decreasing contribution weight; ties by distance to q, then index."""
-    return sorted(range(len(wbar)), key=lambda j: (-float(wbar[j]), abs(j - q), j))
+    """Partitions by decreasing contribution weight; equal weights by distance
+    to the query partition q, then by index (numpy's stable lexicographic
+    sort, whose last key is the primary one)."""
+    w = np.asarray(wbar, dtype=np.float64)
+    idx = np.arange(w.size)
+    return [int(j) for j in np.lexsort((idx, np.abs(idx - q), -w))]
 
 
 def plan_threshold(wbar: Sequence[float], q: int, thr: float) -> List[int]:
     """Mask of partitions to compute: q, and every j with weight strictly above thr."""
-    return [1 if (j == q or float(wbar[j]) > thr) else 0 for j in range(len(wbar))]
+    m = (np.asarray(wbar, dtype=np.float64) > float(thr)).astype(np.int64)
+    m[q] = 1
+    return [int(x) for x in m]
 
 
 class AnchorPlanner:

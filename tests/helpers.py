@@ -51,3 +51,16 @@ def max_abs(a, b) -> float:
     with np.errstate(invalid="ignore"):
         d = np.where(both_inf, 0.0, np.abs(a - b))
     return float(np.nanmax(d)) if d.size else 0.0
+
+
+def per_head(fn, H: int, workers: int = 0):
+    """fn(h) for every head h, in a thread pool; heads are independent in
+    every oracle function, so the results are those of one call over all
+    heads.  NumPy's matrix products and exponentials release the GIL; BLAS
+    runs one thread per task."""
+    import concurrent.futures as cf
+    import os
+    from threadpoolctl import threadpool_limits
+    n = workers or max(1, min(H, len(os.sched_getaffinity(0)), 16))
+    with threadpool_limits(1), cf.ThreadPoolExecutor(n) as ex:
+        return list(ex.map(fn, range(H)))

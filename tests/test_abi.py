@@ -72,6 +72,12 @@ def test_attn_argument_validation(L):
     assert attn(L, offs=(1, 6, 10), sel=(1, 1)) == 1      # offsets[0] != 0
     assert attn(L, scale=float("nan")) == 1
     assert attn(L, scale=float("inf")) == 1
+    # the kernels need scale > 0: masked tail keys are -inf before scaling
+    # and the running maximum is taken over unscaled scores
+    assert attn(L, scale=0.0) == 1
+    assert attn(L, scale=-0.0) == 1
+    assert attn(L, scale=-0.125) == 1
+    assert attn(L, scale=float("-inf")) == 1
     big = tuple(range(66))
     assert attn(L, offs=big, sel=(1,) * 65) == 2          # more than 64 partitions
 

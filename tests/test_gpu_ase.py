@@ -1,8 +1,10 @@
 """GPU parity of the error-model selection (Alg. 1 with group states) on the
 reduced planner workload: state norms against float64, then per step the
 anchor decision, the computed groups and the composed output against the
-float64 oracle following the same rule (decisions compared exactly unless the
-oracle's margin to a threshold is within 2 %)."""
+float64 oracle following the same rule.  Decisions are compared exactly
+unless the oracle's own margin of the decision that differs is within 2 %;
+the oracle then takes the GPU's decision and the comparison goes on, so
+every step is checked."""
 import numpy as np
 import pytest
 
@@ -48,7 +50,7 @@ def test_error_model_planner_reduced():
         steps.append(gen_evolved(w, steps[-1], s))
     offs = w.offsets
     tol = TOL["bf16"]
-    reused_total = 0
+    reused_total = resync = 0
     for qb in (3, 6):
         em = ErrorModelSelectiveAttention(w.B, w.H, w.D, offs, qb, G, w.scale, R, EPS_LOCAL, torch.bfloat16)
         gpu = []
@@ -56,20 +58,42 @@ def test_error_model_planner_reduced():
             q, k, v = (to_gpu(xs[n], "bf16") for n in ("q", "k", "v"))
             out, lse, info = em.step(t, q, k, v)
             gpu.append((info["anchor"], list(info["compute"]), out.float().cpu().numpy(), lse.cpu().numpy()))
-        orc = ase_planner.run([{n: exact_inputs(v_, "bf16") for n, v_ in xs.items()} for xs in steps],
-                              offs, qb, G, R, EPS_LOCAL, w.scale)
-        for t in range(w.steps):
+        X = [{n: exact_inputs(v_, "bf16") for n, v_ in xs.items()} for xs in steps]
+        force = {}
+        orc = ase_planner.run(X, offs, qb, G, R, EPS_LOCAL, w.scale)
+        t = 0
+        while t < w.steps:
             ga, gc, go, gl = gpu[t]
             o = orc[t]
             if (ga, gc) != (o["anchor"], o["compute"]):
-                eps = o["eps"]
-                # the group whose ASE defines eps (the quantile) decides identically on both sides
-                margins = [abs(v_ - eps) / max(eps, 1e-30) for v_ in o["ase"].values() if v_ != eps]
-                if o["drift"] is not None:
-                    margins.append(abs(o["drift"] - EPS_LOCAL) / EPS_LOCAL)
-                assert min(margins) <= 0.02, (qb, t, ga, gc, o["anchor"], o["compute"], min(margins))
-                break
+                m = differing_margin(o, ga, gc)
+                assert m <= 0.02, (qb, t, ga, gc, o["anchor"], o["compute"], m)
+                # re-synchronise: the oracle takes the GPU's decision here
+                force[t] = (ga, gc)
+                resync += 1
+                orc = ase_planner.run(X, offs, qb, G, R, EPS_LOCAL, w.scale, force=force)
+                continue
             reused_total += len(em.groups) - len(gc)
             assert max_abs(go, o["out"]) <= tol["out"], (qb, t)
             assert max_abs(gl, o["lse"]) <= tol["lse"], (qb, t)
+            t += 1
+    print(f"reused groups {reused_total}, oracle re-synchronised {resync} times", flush=True)
     assert reused_total > 0
+
+
+def differing_margin(o, ga, gc):
+    """Relative margin, in the oracle, of the decision on which the GPU
+    differs.  The anchor rule is (every group's ASE above eps) or (relative
+    local drift above eps_local): if the oracle anchors, every condition that
+    holds must be near its threshold for the GPU not to; if it does not, one
+    of the two must be.  Otherwise every group computed on one side only must
+    have its ASE near eps."""
+    eps = max(o["eps"], 1e-30)
+    c_ase = (min(o["ase"].values()) - o["eps"]) / eps
+    c_drift = (o["drift"] - EPS_LOCAL) / EPS_LOCAL
+    if ga != o["anchor"]:
+        if o["anchor"]:
+            return max([abs(c) for c in (c_ase, c_drift) if c > 0], default=float("inf"))
+        return min(abs(c_ase), abs(c_drift))
+    diff = set(gc) ^ set(o["compute"])
+    return max(abs(o["ase"][grp] - o["eps"]) / eps for grp in diff)

@@ -1,7 +1,9 @@
 """GPU parity of the planner-driven multi-step workload on a reduced shape
 (2 heads, 16,384 tokens, 8 partitions, every query block, 10 steps, anchors
-at steps 0 and 5, threshold 0.05 on the anchor weights): selections, composed
-outputs, LSE and weights against the float64 oracle following the same rule."""
+at steps 0 and 5, threshold 1/8 on the anchor weights): selections, composed
+outputs, LSE and weights against the float64 oracle following the same rule.
+Every step of every block is compared: a mask that differs on a near-tie
+re-synchronises the oracle to the GPU's mask."""
 import numpy as np
 import pytest
 
@@ -41,21 +43,33 @@ def test_planner_workload_reduced():
             res[qb] = (mask, out.float().cpu().numpy(), lse.cpu().numpy(), wp_h)
         gpu.append(res)
 
-    orc = multistep.run([{k: exact_inputs(v, "bf16") for k, v in xs.items()} for xs in steps],
-                        offs, blocks, w.anchors, w.threshold, w.scale)
+    # the oracle per query block (blocks are independent); a mask that
+    # differs is allowed only where every differing partition's anchor weight
+    # sits within the weight tolerance of the threshold, and the oracle is
+    # then re-run with the GPU's mask so that the later steps stay checked
+    X = [{k: exact_inputs(v, "bf16") for k, v in xs.items()} for xs in steps]
     tol = TOL["bf16"]
-    n_reused = 0
-    for s in range(w.steps):
-        for qb in blocks:
+    n_reused = n_resync = 0
+    for qb in blocks:
+        force = {}
+        s = 0
+        orc = multistep.run(X, offs, [qb], w.anchors, w.threshold, w.scale)
+        while s < w.steps:
             gm, go, gl, gw = gpu[s][qb]
             om, oo, ol, ow = orc[s][qb]
             if gm != om:
-                # allowed only where the anchor weight sits within tolerance of the threshold
-                margin = min(abs(x - w.threshold) for x in orc[max(a for a in w.anchors if a <= s)][qb][3])
+                anchor_w = orc[max(a for a in w.anchors if a <= s)][qb][3]
+                diff = [j for j in range(w.P) if gm[j] != om[j]]
+                margin = max(abs(anchor_w[j] - w.threshold) for j in diff)
                 assert margin <= tol["w"], (s, qb, gm, om, margin)
+                force[(s, qb)] = gm
+                n_resync += 1
+                orc = multistep.run(X, offs, [qb], w.anchors, w.threshold, w.scale, force=force)
                 continue
             n_reused += w.P - sum(gm)
             assert max_abs(go, oo) <= tol["out"], (s, qb)
             assert max_abs(gl, ol) <= tol["lse"], (s, qb)
             assert max_abs(gw, ow) <= tol["w"], (s, qb)
+            s += 1
+    print(f"reused slots {n_reused}, oracle re-synchronised {n_resync} times", flush=True)
     assert n_reused > 0          # the run really reused cached states

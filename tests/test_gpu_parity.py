@@ -18,7 +18,7 @@ import oracle
 from fixtures import gen_qkv, get_workload, sample_rows
 from fixtures.workloads import Workload, partition_offsets
 
-from helpers import TOL, exact_inputs, max_abs, new_state_cache, to_gpu, torch_dtype
+from helpers import TOL, exact_inputs, max_abs, new_state_cache, per_head, to_gpu, torch_dtype
 
 pytestmark = pytest.mark.gpu
 
@@ -65,27 +65,39 @@ def run_step(w, x, select, rows_prev=True):
 
 
 def oracle_step(w, x, select, rows):
-    """Oracle on query rows ``rows`` of the query block (rows are independent)."""
+    """Oracle on query rows ``rows`` of the query block (rows and heads are
+    independent: the heads run in parallel and are stacked back)."""
     offs = w.offsets
     qa, qb = offs[w.q], offs[w.q + 1]
-    X = {k: exact_inputs(v, w.dtype) for k, v in x.items()}
-    qrow = lambda name: X[name][:, qa:qb][:, rows]
     sel = [1 if j in select else 0 for j in range(w.P)]
-    if "q_prev" in X:
-        out, lse, outs, lses = oracle.selective_step(
-            qrow("q"), X["k"], X["v"], qrow("q_prev"), X["k_prev"], X["v_prev"], offs, sel, w.scale)
-    else:
-        outs, lses = oracle.partition_states(qrow("q"), X["k"], X["v"], offs, w.scale)
-        out, lse = oracle.merge(outs, lses)
+
+    def one(h):
+        # the exact input values of head h only (float64 copies per head)
+        qrow = lambda name: exact_inputs(x[name][:, qa:qb][:, rows][:, :, h:h + 1], w.dtype)
+        kv = lambda name: exact_inputs(x[name][:, :, h:h + 1], w.dtype)
+        if "q_prev" in x:
+            _, _, outs, lses = oracle.selective_step(
+                qrow("q"), kv("k"), kv("v"), qrow("q_prev"), kv("k_prev"), kv("v_prev"), offs, sel, w.scale)
+        else:
+            outs, lses = oracle.partition_states(qrow("q"), kv("k"), kv("v"), offs, w.scale)
+        return outs, lses
+
+    parts = per_head(one, w.H)
+    outs = [np.concatenate([p[0][j] for p in parts], axis=2) for j in range(w.P)]
+    lses = [np.concatenate([p[1][j] for p in parts], axis=1) for j in range(w.P)]
+    out, lse = oracle.merge(outs, lses)
     W, wbar = oracle.contrib(lses, lse)
     return dict(outs=outs, lses=lses, out=out, lse=lse, W=W, wbar=wbar)
 
 
 def compare(w, g, o, rows, tol, check_wbar=True):
-    """Slot states, composed state and per-row weights at ``rows``; the
-    per-partition means against the oracle when ``rows`` are all rows, else
-    against the float64 mean of the GPU's own per-row weights over all rows
-    (the oracle only sees the sampled rows)."""
+    """Slot states, composed state and per-row weights at ``rows``, and the
+    per-partition mean weights with their ranking (R3: exact wherever the
+    oracle's adjacent gap exceeds the weight tolerance).  With all rows the
+    GPU's w_part is compared with the oracle's mean; with sampled rows the
+    GPU's per-row weights are averaged over the same rows as the oracle's,
+    and w_part is checked to be the mean of the GPU's per-row weights over
+    all rows."""
     sampled = len(rows) < w.q_len
     worst = {}
     for j in range(w.P):
@@ -100,10 +112,15 @@ def compare(w, g, o, rows, tol, check_wbar=True):
     assert e_lse <= tol["lse"], ("merged", e_lse)
     e_w = max_abs(g["w_rows"][:, :, rows], o["W"])
     assert e_w <= 2 * tol["lse"] + 1e-6, ("w_rows", e_w)
-    if check_wbar and not sampled:
+    if not check_wbar:
+        return worst
+    if not sampled:
         assert max_abs(g["w_part"], o["wbar"]) <= tol["w"]
         check_ranking(g["w_part"], o["wbar"], w.q, tol["w"])
-    elif check_wbar:
+    else:
+        g_mean = g["w_rows"][:, :, rows].astype(np.float64).reshape(-1, w.P).mean(axis=0)
+        assert max_abs(g_mean, o["wbar"]) <= tol["w"], ("sampled wbar", g_mean, o["wbar"])
+        check_ranking(g_mean, o["wbar"], w.q, tol["w"])
         full_mean = g["w_rows"].astype(np.float64).reshape(-1, w.P).mean(axis=0)
         assert max_abs(g["w_part"], full_mean) <= 1e-5
     return worst
@@ -159,12 +176,17 @@ def test_videodit_bf16_sampled_rows():
 
 
 @pytest.mark.slow
-def test_longctx_bf16_sampled_rows_k4():
+@pytest.mark.parametrize("k", [4, 16])
+def test_longctx_bf16_sampled_rows(k):
+    """Nearest-first selections of 4 and of all 16 partitions (16 = full
+    attention over 131,072 keys), 1024 sampled rows."""
+    from fixtures.workloads import nearest_first
     w = get_workload("longctx_bf16_h24_d128_s131072_p16")
-    x = gen_qkv(w)
-    g = run_step(w, x, w.select)
-    rows = sample_rows(w.q_len, 384, w.seed)
-    o = oracle_step(w, x, w.select, rows)
+    select = tuple(nearest_first(w.P, w.q, k))
+    x = gen_qkv(w, with_prev=k < w.P)
+    g = run_step(w, x, select)
+    rows = sample_rows(w.q_len, 1024, w.seed)
+    o = oracle_step(w, x, select, rows)
     compare(w, g, o, rows, TOL["bf16"])
 
 
@@ -173,7 +195,7 @@ def test_hunyuan_d64_bf16_sampled_rows():
     w = get_workload("hunyuan_bf16_h48_d64_s118800_p8")
     x = gen_qkv(w)
     g = run_step(w, x, w.select)
-    rows = sample_rows(w.q_len, 256, w.seed)
+    rows = sample_rows(w.q_len, 1024, w.seed)
     o = oracle_step(w, x, w.select, rows)
     compare(w, g, o, rows, TOL["bf16"])
 
@@ -183,7 +205,7 @@ def test_videodit_cfg_batch2_sampled_rows():
     w = get_workload("videodit_cfg_bf16_b2_h40_d128_s75600_p8")
     x = gen_qkv(w)
     g = run_step(w, x, w.select)
-    rows = sample_rows(w.q_len, 256, w.seed)
+    rows = sample_rows(w.q_len, 1024, w.seed)
     o = oracle_step(w, x, w.select, rows)
     compare(w, g, o, rows, TOL["bf16"])
 
@@ -259,6 +281,70 @@ def test_ragged_shapes(dtype, D, H, q_len, lens):
             for j in range(P):
                 assert max_abs(s2[j].float().cpu().numpy(), outs[j]) <= tol["out"], j
                 assert max_abs(l2[j].cpu().numpy(), lses[j]) <= tol["lse"], j
+
+
+@pytest.mark.parametrize("dtype,D", [("bf16", 128), ("bf16", 64), ("f32", 64)])
+def test_twenty_partitions_attn_merge_contrib(dtype, D):
+    """P = 20 (three of them empty): the attention launch over 17 selected
+    partitions, the merge of all 20 slots and the weights of 20 partitions
+    run the instantiations for more than 16 slots; every result against the
+    oracle, the ranking by R3, and a 17-slot subset list."""
+    import torch
+    a = api()
+    rng = np.random.default_rng(20 + D)
+    lens = [33, 0, 64, 65, 1, 190, 0, 96, 97, 5, 128, 200, 7, 0, 63, 129, 40, 2, 250, 31]
+    P = len(lens)
+    offs = [0]
+    for n in lens:
+        offs.append(offs[-1] + n)
+    S = offs[-1]
+    B, H, q_len = 1, 2, 301
+    q = rng.standard_normal((B, q_len, H, D), dtype=np.float32)
+    k = rng.standard_normal((B, S, H, D), dtype=np.float32) + 0.25
+    v = rng.standard_normal((B, S, H, D), dtype=np.float32)
+    # key norms differ per partition so that the weights are well separated
+    k *= np.repeat(np.linspace(0.3, 1.6, P), lens).astype(np.float32)[None, :, None, None]
+    scale = 1 / math.sqrt(D)
+    qg, kg, vg = (to_gpu(t, dtype) for t in (q, k, v))
+    mask = [1] * P
+    st, ls = new_state_cache(P, B, q_len, H, D, dtype)
+    n_ws = a.attn_workspace_bytes(torch_dtype(dtype), B, H, D, q_len, offs, mask)
+    ws_attn = torch.empty(n_ws, dtype=torch.uint8, device="cuda") if n_ws > 0 else None
+    a.attn_partition_states(qg, kg, vg, offs, mask, scale, st, ls, ws_attn)
+    out = torch.empty((B, q_len, H, D), dtype=torch_dtype(dtype), device="cuda")
+    lse = torch.empty((B, H, q_len), dtype=torch.float32, device="cuda")
+    a.merge_states(st, ls, out, lse)
+    sub = [19, 0, 2, 3, 4, 5, 7, 8, 9, 10, 11, 12, 14, 15, 16, 17, 18]      # 17 slots, empty ones left out
+    out_s = torch.empty_like(out)
+    lse_s = torch.empty_like(lse)
+    a.merge_states(st, ls, out_s, lse_s, slots=sub)
+    w_part = torch.empty(P, dtype=torch.float32, device="cuda")
+    w_rows = torch.empty((B, H, q_len, P), dtype=torch.float32, device="cuda")
+    cws = torch.empty(a.contrib_workspace_bytes(B, H, q_len, P), dtype=torch.uint8, device="cuda")
+    a.contrib(ls, lse, w_part, cws, w_rows)
+    torch.cuda.synchronize()
+    Q, K, V = (exact_inputs(t, dtype) for t in (q, k, v))
+    outs, lses = oracle.partition_states(Q, K, V, offs, scale)
+    tol = TOL[dtype]
+    for j in range(P):
+        go, gl = st[j].float().cpu().numpy(), ls[j].cpu().numpy()
+        if lens[j] == 0:
+            assert np.all(np.isneginf(gl)) and np.all(go == 0), j
+        assert max_abs(go, outs[j]) <= tol["out"], j
+        assert max_abs(gl, lses[j]) <= tol["lse"], j
+    mo, ml = oracle.merge(outs, lses)
+    assert max_abs(out.float().cpu().numpy(), mo) <= tol["out"]
+    assert max_abs(lse.cpu().numpy(), ml) <= tol["lse"]
+    # the empty partitions carry weight 0: the subset composes to the same state
+    so, sl = oracle.merge([outs[j] for j in sub], [lses[j] for j in sub])
+    assert max_abs(out_s.float().cpu().numpy(), so) <= tol["out"]
+    assert max_abs(lse_s.cpu().numpy(), sl) <= tol["lse"]
+    W, wbar = oracle.contrib(lses, ml)
+    assert max_abs(w_rows.cpu().numpy(), W) <= 2 * tol["lse"] + 1e-6
+    wp = w_part.cpu().numpy()
+    assert max_abs(wp, wbar) <= tol["w"]
+    assert all(wp[j] == 0.0 for j in range(P) if lens[j] == 0)
+    check_ranking(wp, wbar, 9, tol["w"])
 
 
 @pytest.mark.parametrize("D", [128, 64])

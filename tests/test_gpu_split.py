@@ -56,7 +56,9 @@ def test_tail_split_matches_oracle_and_unsplit(D, lens, select, state_dt):
 
     need = a.attn_workspace_bytes(torch.bfloat16, B, H, D, q_len, offs, mask)
     print(f"split case D={D} lens={lens} q_len={q_len} tasks={q_tiles * per_tile} cus={cus} ws={need}", flush=True)
-    assert need > 0, "one full round plus 16 tasks must split the tail"
+    # more than the 256 bytes of queue counters: the plan asks for the
+    # partial states of a split tail
+    assert need > 256, "one full round plus 16 tasks must split the tail"
     ws = torch.empty(need, dtype=torch.uint8, device="cuda")
 
     sdt = torch.float32 if state_dt == "f32" else torch.bfloat16
@@ -83,6 +85,9 @@ def test_tail_split_matches_oracle_and_unsplit(D, lens, select, state_dt):
     for s_b, l_b in ((s_small, l_small), (s_queue, l_queue)):
         assert torch.equal(s_b.view(torch.uint8), s_plain.view(torch.uint8))
         assert torch.equal(l_b.view(torch.int32), l_plain.view(torch.int32))
+    # the split path really ran: the composed key ranges round differently
+    # from the single pass somewhere in the split tasks' rows
+    assert not torch.equal(l_split.view(torch.int32), l_plain.view(torch.int32))
     # unselected slots untouched
     ity = torch.int16 if sdt == torch.bfloat16 else torch.int32
     for j in range(P):

@@ -15,6 +15,8 @@ What fixes the expected values:
   of Eq. scale_ratio and the local drift of Eq. error_extrapolation) is
   exactly c * sum_{j in G} w_j ||OUT_j||.
 """
+import math
+
 import numpy as np
 import pytest
 
@@ -161,3 +163,91 @@ def test_error_planner_closed_forms_under_a_value_scaling(c):
         assert ase == pytest.approx(expect, rel=1e-10)
     # a relative local drift above eps_local makes the step an anchor (Sec. 4.2.4)
     assert r["anchor"] == (c > eps_local)
+
+
+# ---- several anchors: the eps adaptation, group snapshots and corrections
+#
+# Q and K fixed, V_t = (1 + c_t) V_0.  No LSE moves, so every anchor weight
+# stays w_j (step 0's), every partition and group output is (1 + c_t) times
+# its step-0 value, and with A_G = sum_{j in G} w_j ||OUT_0(j)|| and
+# B_G = w(G) ||OUT_0(G)||, w(G) = sum_{j in G} w_j:
+#   ASE_t(G)        = |c_t - c_{t_c(G)}| A_G           (local snapshot at t_c)
+#   relative drift  = |c_t - c_{t_a}| / (1 + c_{t_a})
+#   correction(G)   = |c_t - c_{t_c(G)}| B_G           (at an anchor t)
+#   composed LSE    = the full-attention LSE at every step.
+# The step-0 quantities come from torch's float64 attention and scipy's
+# logsumexp over each partition's and group's key range, not from the oracle.
+
+def _truth_by_key_range(x, offs, q, scale):
+    torch = pytest.importorskip("torch")
+    from scipy.special import logsumexp
+    Q = x["q"][:, offs[q]:offs[q + 1]]
+
+    def out(a, e):
+        t = lambda y: torch.from_numpy(np.ascontiguousarray(y)).permute(0, 2, 1, 3)
+        o = torch.nn.functional.scaled_dot_product_attention(t(Q), t(x["k"][:, a:e]), t(x["v"][:, a:e]), scale=scale)
+        return o.permute(0, 2, 1, 3).numpy()
+
+    def lse(a, e):
+        return logsumexp(scale * np.einsum("brhd,bchd->bhrc", Q, x["k"][:, a:e]), axis=-1)
+
+    return out, lse
+
+
+def test_error_planner_eps_adaptation_over_several_anchors():
+    S, P, q, scale, g, R, eps_local = 40, 8, 3, 0.35, 2, 0.5, 0.1
+    offs = partition_offsets(S, P)
+    x0 = seq(7)
+    c = [0.0, 0.05, 0.08, 0.3, 0.32, 0.6, 0.62]
+    xs = [dict(x0, v=x0["v"] * (1.0 + ct)) for ct in c]
+    res = ase_planner.run(xs, offs, q, g, R, eps_local, scale)
+
+    out_of, lse_of = _truth_by_key_range(x0, offs, q, scale)
+    lse_full = lse_of(0, S)
+    w = [float(np.mean(np.exp(lse_of(offs[j], offs[j + 1]) - lse_full))) for j in range(P)]
+    n_part = [float(np.linalg.norm(out_of(offs[j], offs[j + 1]))) for j in range(P)]
+    groups = og.groups_of(P, q, g)
+    assert groups == [(0, 2), (2, 3), (4, 6), (6, 8)]
+    A = {G: sum(w[j] * n_part[j] for j in range(*G)) for G in groups}
+    Bc = {G: sum(w[j] for j in range(*G)) * float(np.linalg.norm(out_of(offs[G[0]], offs[G[1]]))) for G in groups}
+
+    # the rule, followed on the closed forms: eps from step 1's ASE until
+    # the first correction errors exist, then their R-quantile
+    # (sorted[ceil(R m) - 1]) over every anchor so far
+    quant = lambda v: sorted(v)[int(math.ceil(R * len(v))) - 1]
+    t_c, t_a, eps, corr = {G: 0 for G in groups}, 0, None, []
+    anchors = []
+    for t in range(1, len(c)):
+        r = res[t]
+        ase = {G: abs(c[t] - c[t_c[G]]) * A[G] for G in groups}
+        drift = abs(c[t] - c[t_a]) / (1.0 + c[t_a])
+        assert r["drift"] == pytest.approx(drift, rel=1e-9, abs=1e-15)
+        for G in groups:
+            assert r["ase"][G] == pytest.approx(ase[G], rel=1e-9, abs=1e-15), (t, G)
+        if eps is None:
+            eps = quant(list(ase.values()))
+        anchor = all(v > eps for v in ase.values()) or drift > eps_local
+        assert r["anchor"] == anchor, t
+        if anchor:
+            corr += [abs(c[t] - c[t_c[G]]) * Bc[G] for G in groups]
+            eps = quant(corr)
+            t_c, t_a = {G: t for G in groups}, t
+            anchors.append(t)
+        else:
+            comp = [G for G in groups if ase[G] > eps]
+            assert r["compute"] == comp, t
+            for G in comp:
+                t_c[G] = t
+        assert r["eps"] == pytest.approx(eps, rel=1e-9), t
+        assert r["t_c"] == t_c, t
+        np.testing.assert_allclose(r["corrections"], corr, rtol=1e-9)
+        # no LSE moved: the composed LSE is full attention's at every step
+        np.testing.assert_allclose(r["lse"], lse_full, rtol=1e-12)
+
+    # the schedule reaches every branch: groups recomputed between anchors
+    # (three different snapshot steps at the second anchor), two anchors
+    # after the first, and a quantile over the corrections of both
+    assert anchors == [3, 5]
+    assert sorted(set(res[2]["t_c"].values())) == [0, 1, 2]
+    assert len(res[5]["corrections"]) == 8 and len(res[4]["corrections"]) == 4
+    assert res[5]["eps"] == pytest.approx(sorted(res[5]["corrections"])[3], rel=0)

@@ -66,3 +66,32 @@ def test_quantile_rule_matches_oracle():
     assert quantile_r([3.0, 1.0, 2.0, 4.0], 0.5) == 2.0
     assert quantile_r([3.0, 1.0, 2.0, 4.0], 0.75) == 3.0
     assert quantile_r([3.0], 0.1) == 3.0
+
+
+def test_product_rank_hand_examples():
+    # decreasing weight; equal weights by distance to q, then by index
+    assert planner.rank_partitions([0.1, 0.3, 0.3, 0.2, 0.1], 2) == [2, 1, 3, 0, 4]
+    assert planner.rank_partitions([0.25] * 4, 1) == [1, 0, 2, 3]
+    assert planner.rank_partitions([0.5, 0.0, 0.5], 2) == [2, 0, 1]
+    assert planner.rank_partitions([0.0, 0.1, 0.2, 0.3, 0.4], 0) == [4, 3, 2, 1, 0]
+    assert planner.rank_partitions([0.7], 0) == [0]
+
+
+def test_product_threshold_hand_examples():
+    # strictly above the threshold, and the query partition always
+    assert planner.plan_threshold([0.05, 0.050001, 0.2, 0.0], 3, 0.05) == [0, 1, 1, 1]
+    assert planner.plan_threshold([0.05, 0.050001, 0.2, 0.0], 3, 0.3) == [0, 0, 0, 1]
+    assert planner.plan_threshold([0.4, 0.3, 0.3], 0, 0.0) == [1, 1, 1]
+    assert planner.plan_threshold([0.0, 0.0, 0.0], 1, 0.0) == [0, 1, 0]
+
+
+def test_product_quantile_hand_examples():
+    from paper_2607_15650_amd.ase import quantile_r
+    v = [4.0, 1.0, 3.0, 2.0]
+    assert quantile_r(v, 0.0) == 1.0          # the smallest
+    assert quantile_r(v, 0.25) == 1.0         # ceil(1) = 1st
+    assert quantile_r(v, 0.26) == 2.0         # ceil(1.04) = 2nd
+    assert quantile_r(v, 0.5) == 2.0
+    assert quantile_r(v, 0.51) == 3.0
+    assert quantile_r(v, 1.0) == 4.0
+    assert quantile_r([0.3, 0.1, 0.2, 0.9, 0.5, 0.7, 0.8, 0.6], 0.5) == 0.5   # 4th of 8
