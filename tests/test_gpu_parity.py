@@ -330,7 +330,15 @@ def test_twenty_partitions_attn_merge_contrib(dtype, D):
         go, gl = st[j].float().cpu().numpy(), ls[j].cpu().numpy()
         if lens[j] == 0:
             assert np.all(np.isneginf(gl)) and np.all(go == 0), j
-        assert max_abs(go, outs[j]) <= tol["out"], j
+        # a partition of a few keys has OUT of the size of one V row: its bf16
+        # state carries the store rounding 2^-8 |OUT| and the rounding of the
+        # probabilities in the P.V product, up to 2^-8 max|v|, which at unit
+        # variance can exceed 1e-2 (the bar assumes OUT averaged over many keys)
+        t_out = tol["out"]
+        if dtype == "bf16" and lens[j] > 0:
+            vmax = float(np.abs(V[:, offs[j]:offs[j + 1]]).max())
+            t_out = max(t_out, 2.0 ** -8 * (float(np.abs(outs[j]).max()) + vmax) + 2.0 ** -12)
+        assert max_abs(go, outs[j]) <= t_out, (j, max_abs(go, outs[j]), t_out)
         assert max_abs(gl, lses[j]) <= tol["lse"], j
     mo, ml = oracle.merge(outs, lses)
     assert max_abs(out.float().cpu().numpy(), mo) <= tol["out"]
