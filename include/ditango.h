@@ -206,6 +206,31 @@ ditango_status ditango_contrib(
     int B, int H, int64_t q_len,
     float* w_rows, float* w_part, void* workspace, void* stream);
 
+/* Size of the fixed device scratch array of ditango_contrib_noalloc. */
+#define DITANGO_CONTRIB_SCRATCH_BYTES (1u << 20)
+
+/*
+ * ditango_contrib without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.  Same arguments (minus the workspace),
+ * same kernels and results bit for bit as ditango_contrib.  Allocates
+ * nothing: the per-workgroup partial sums go to a fixed device array of
+ * DITANGO_CONTRIB_SCRATCH_BYTES bytes (one per GPU, held until the process
+ * ends; its address is looked up on a device's first call).
+ *
+ * Limit: ditango_contrib_workspace_bytes(B, H, q_len, P) must not exceed
+ * DITANGO_CONTRIB_SCRATCH_BYTES (e.g. up to about 16.7 million rows
+ * B*H*q_len at P = 8, 2.1 million at P = 64); larger sizes return
+ * DITANGO_ERR_UNSUPPORTED before anything is launched.  Every call on one GPU
+ * shares that array: calls that overlap on one GPU (on different streams or
+ * from several threads) race.  Nothing in the array needs to start at zero:
+ * every partial sum a call reads is written earlier in the same call.
+ */
+ditango_status ditango_contrib_noalloc(
+    const float* lse_states, const float* lse_out, int P,
+    int B, int H, int64_t q_len,
+    float* w_rows, float* w_part, void* stream);
+
 /*
  * Bytes of device workspace ditango_state_norms needs for these sizes.
  */

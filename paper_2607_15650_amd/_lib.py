@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(HERE, "libditango.so")
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_HIP = 0, 1, 2, 3
 F32, BF16 = 0, 1
 MAX_PARTITIONS = 64
+CONTRIB_SCRATCH_BYTES = 1 << 20
 
 # Every symbol include/ditango.h declares, with (restype, argtypes).
 _c = ctypes
@@ -48,6 +49,10 @@ SIGNATURES = {
         _c.c_void_p, _c.c_void_p, _c.c_int,
         _c.c_int, _c.c_int, _c.c_int64,
         _c.c_void_p, _c.c_void_p, _c.c_void_p, _c.c_void_p]),
+    "ditango_contrib_noalloc": (_c.c_int, [
+        _c.c_void_p, _c.c_void_p, _c.c_int,
+        _c.c_int, _c.c_int, _c.c_int64,
+        _c.c_void_p, _c.c_void_p, _c.c_void_p]),
     "ditango_norms_workspace_bytes": (_c.c_size_t, [_c.c_int, _c.c_int, _c.c_int, _c.c_int64, _c.c_int]),
     "ditango_state_norms": (_c.c_int, [
         _c.c_void_p, _c.c_int, _c.c_int, _c.POINTER(_c.c_int32), _c.c_int,

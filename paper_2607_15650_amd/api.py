@@ -162,6 +162,24 @@ def contrib(lse_states: torch.Tensor, lse_out: torch.Tensor, w_part: torch.Tenso
     _lib.check("ditango_contrib", st)
 
 
+def contrib_noalloc(lse_states: torch.Tensor, lse_out: torch.Tensor, w_part: torch.Tensor,
+                    w_rows: Optional[torch.Tensor] = None) -> None:
+    """ditango_contrib_noalloc: the weights with the library's fixed device
+    scratch instead of a workspace (nothing is allocated)."""
+    _dev(lse_states, lse_out, w_part, w_rows)
+    P, B, H, q_len = lse_states.shape
+    if tuple(lse_out.shape) != (B, H, q_len):
+        raise ValueError("lse_out must be [B, H, q_len]")
+    if tuple(w_part.shape) != (P,) or w_part.dtype != torch.float32:
+        raise ValueError("w_part must be float32 [P]")
+    if w_rows is not None and (tuple(w_rows.shape) != (B, H, q_len, P) or w_rows.dtype != torch.float32):
+        raise ValueError("w_rows must be float32 [B, H, q_len, P]")
+    st = _lib.lib().ditango_contrib_noalloc(
+        lse_states.data_ptr(), lse_out.data_ptr(), P, B, H, q_len,
+        w_rows.data_ptr() if w_rows is not None else None, w_part.data_ptr(), _stream())
+    _lib.check("ditango_contrib_noalloc", st)
+
+
 def norms_workspace_bytes(B: int, H: int, D: int, q_len: int, n_slots: int) -> int:
     return int(_lib.lib().ditango_norms_workspace_bytes(B, H, D, q_len, n_slots))
 

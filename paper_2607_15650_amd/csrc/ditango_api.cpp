@@ -202,6 +202,30 @@ ditango_status ditango_contrib(
   return from_hip(launch_contrib(a, (hipStream_t)stream));
 }
 
+ditango_status ditango_contrib_noalloc(
+    const float* lse_states, const float* lse_out, int P,
+    int B, int H, int64_t q_len,
+    float* w_rows, float* w_part, void* stream) {
+  if (!lse_states || !lse_out || !w_part) return DITANGO_ERR_INVALID;
+  if (B < 1 || H < 1 || q_len < 1 || P < 1) return DITANGO_ERR_INVALID;
+  if (P > kMaxParts) return DITANGO_ERR_UNSUPPORTED;
+  // the partial sums must fit the fixed scratch array
+  if (ditango_contrib_workspace_bytes(B, H, q_len, P) > kContribScratchBytes) return DITANGO_ERR_UNSUPPORTED;
+  float* partial = nullptr;
+  if (contrib_scratch(&partial) != hipSuccess) return DITANGO_ERR_HIP;
+  ContribArgs a;
+  memset(&a, 0, sizeof(a));
+  a.lse = lse_states;
+  a.lse_out = lse_out;
+  a.w_rows = w_rows;
+  a.w_part = w_part;
+  a.partial = partial;
+  a.n_rows = (int64_t)B * H * q_len;
+  a.P = P;
+  a.n_blocks = (int)contrib_blocks(a.n_rows);
+  return from_hip(launch_contrib(a, (hipStream_t)stream));
+}
+
 static int64_t norm_blocks(int B, int H, int D, int64_t q_len) {
   const int64_t chunks = (int64_t)B * q_len * H * D / 8;
   return (chunks + kNormChunksPerBlock - 1) / kNormChunksPerBlock;

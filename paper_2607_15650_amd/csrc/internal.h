@@ -151,6 +151,11 @@ hipError_t launch_attn_f32(const AttnArgs& a, int D, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, ditango_dtype sdt, ditango_dtype odt, int D,
                         hipStream_t s);
 hipError_t launch_contrib(const ContribArgs& a, hipStream_t s);
+// Device address, on the current device, of the fixed scratch array of the
+// allocation-free contrib entry point (kContribScratchBytes); looked up once
+// per device.
+constexpr size_t kContribScratchBytes = DITANGO_CONTRIB_SCRATCH_BYTES;
+hipError_t contrib_scratch(float** ptr);
 hipError_t launch_norms(const NormArgs& a, ditango_dtype dt, hipStream_t s);
 
 constexpr int kProbeThreads = 256;   // 4 waves per workgroup

@@ -11,6 +11,8 @@
 // anchor weights of Eq. lse_weight) and their mean over all rows per
 // partition, reduced in a fixed order (workgroup tree, then one workgroup over
 // the per-workgroup partial sums) so results are bitwise reproducible.
+#include <mutex>
+
 #include "internal.h"
 
 namespace ditango {
@@ -282,6 +284,39 @@ hipError_t launch_contrib(const ContribArgs& a, hipStream_t s) {
   if (a.P <= 8) return launch_contrib_t<8>(a, s);
   if (a.P <= 16) return launch_contrib_t<16>(a, s);
   return launch_contrib_t<kMaxParts>(a, s);
+}
+
+// ---- scratch of the allocation-free contrib entry point
+//
+// The per-workgroup partial sums live in a file-scope device array: one copy
+// per GPU, held until the process ends.  In host code `scratch` names a
+// host-side stand-in, not device memory, so its device address is looked up
+// once per device (with that device current) and only that address is
+// passed to kernels.
+static __device__ __align__(256) float scratch[kContribScratchBytes / sizeof(float)];
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices] = {};
+}  // namespace
+
+hipError_t contrib_scratch(float** ptr) {
+  *ptr = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = (float*)g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace ditango

@@ -188,3 +188,25 @@ def test_attn_workspace_bytes_without_a_split(L):
     assert L.ditango_attn_workspace_bytes(1, 1, 2, 96, 10, o, 2, s) == 0
     assert L.ditango_attn_workspace_bytes(1, 0, 2, 128, 10, o, 2, s) == 0
     assert L.ditango_attn_workspace_bytes(1, 1, 2, 128, 10, o, 2, none) == 0
+
+
+def test_contrib_noalloc_validation_before_any_launch(L):
+    """The allocation-free weights call rejects bad arguments and sizes whose
+    partial sums would not fit its fixed device scratch, before touching the
+    GPU."""
+    from paper_2607_15650_amd import _lib
+    f = L.ditango_contrib_noalloc
+    assert _lib.CONTRIB_SCRATCH_BYTES == 1 << 20
+    assert f(None, FAKE, 8, 1, 40, 9450, None, FAKE, None) == 1
+    assert f(FAKE, None, 8, 1, 40, 9450, None, FAKE, None) == 1
+    assert f(FAKE, FAKE, 8, 1, 40, 9450, None, None, None) == 1
+    assert f(FAKE, FAKE, 0, 1, 40, 9450, None, FAKE, None) == 1
+    assert f(FAKE, FAKE, 8, 1, 0, 9450, None, FAKE, None) == 1
+    assert f(FAKE, FAKE, 8, 1, 40, 0, None, FAKE, None) == 1
+    assert f(FAKE, FAKE, 65, 1, 40, 9450, None, FAKE, None) == 2
+    # the largest row count whose partial sums fit, and one workgroup more
+    per_block, P = 512, 8
+    max_blocks = (1 << 20) // (4 * P)
+    assert L.ditango_contrib_workspace_bytes(1, 1, max_blocks * per_block, P) == 1 << 20
+    assert f(FAKE, FAKE, P, 1, 1, max_blocks * per_block + 1, None, FAKE, None) == 2
+    assert f(FAKE, FAKE, 64, 4, 64, 9450, None, FAKE, None) == 2
