@@ -17,15 +17,23 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
 
-template <typename T> __device__ __forceinline__ f32x8 load8(const T* p);
-template <> __device__ __forceinline__ f32x8 load8<__bf16>(const __bf16* p) {
-  return __builtin_convertvector(__builtin_nontemporal_load((const bf16x8*)p), f32x8);
-}
-template <> __device__ __forceinline__ f32x8 load8<float>(const float* p) {
-  const f32x4 a = __builtin_nontemporal_load((const f32x4*)p);
-  const f32x4 b = __builtin_nontemporal_load((const f32x4*)(p + 4));
-  return f32x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-}
+// 8 consecutive elements, loaded in the state type and used as float
+template <typename T> struct Raw8;
+template <> struct Raw8<__bf16> {
+  typedef bf16x8 type;
+  static __device__ __forceinline__ type load(const __bf16* p) { return __builtin_nontemporal_load((const bf16x8*)p); }
+  static __device__ __forceinline__ f32x8 f32(const type& x) { return __builtin_convertvector(x, f32x8); }
+};
+template <> struct Raw8<float> {
+  typedef f32x8 type;
+  static __device__ __forceinline__ type load(const float* p) {
+    const f32x4 a = __builtin_nontemporal_load((const f32x4*)p);
+    const f32x4 b = __builtin_nontemporal_load((const f32x4*)(p + 4));
+    return f32x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  }
+  static __device__ __forceinline__ f32x8 f32(const type& x) { return x; }
+};
+
 
 // grid: (blocks per slot, n_slots).  Each workgroup sums the squares of a fixed
 // range of 8-element chunks of one slot into partial[slot][block].
@@ -38,14 +46,41 @@ __global__ __launch_bounds__(kNormThreads) void norms_partial_kernel(const NormA
   const T* __restrict__ ref = (const T*)a.ref;
   const int64_t chunks = a.elems / 8;
   const int64_t c0 = (int64_t)blockIdx.x * kNormChunksPerBlock;
+  // batches of kBatch chunks: every load of a batch (state and reference)
+  // is issued before the first is used, and unconditionally (a chunk past
+  // the end reads the last chunk and is then replaced by zeros, which leave
+  // the sum's bits alone): a load under a per-lane condition is waited for
+  // inside its branch.  Chunks stay in the state type until they are used.
+  constexpr int kPer = kNormChunksPerBlock / kNormThreads;
+  constexpr int kBatch = 8;
+  static_assert(kPer % kBatch == 0, "batches");
+  using R = Raw8<T>;
   float sum = 0.f;
-  for (int i = 0; i < kNormChunksPerBlock / kNormThreads; ++i) {
-    const int64_t c = c0 + (int64_t)i * kNormThreads + tid;
-    if (c < chunks) {
-      f32x8 x = load8<T>(src + c * 8);
-      if (ref != nullptr) x -= load8<T>(ref + c * 8);
+#pragma unroll 1
+  for (int i0 = 0; i0 < kPer; i0 += kBatch) {
+    typename R::type x[kBatch], y[kBatch];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sum = __builtin_fmaf(x[e], x[e], sum);
+    for (int i = 0; i < kBatch; ++i) {
+      const int64_t c = c0 + (int64_t)(i0 + i) * kNormThreads + tid;
+      x[i] = R::load(src + (c < chunks ? c : chunks - 1) * 8);
+    }
+    if (ref != nullptr) {
+#pragma unroll
+      for (int i = 0; i < kBatch; ++i) {
+        const int64_t c = c0 + (int64_t)(i0 + i) * kNormThreads + tid;
+        y[i] = R::load(ref + (c < chunks ? c : chunks - 1) * 8);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+      const bool ok = c0 + (int64_t)(i0 + i) * kNormThreads + tid < chunks;
+      f32x8 v = R::f32(x[i]);
+      if (ref != nullptr) v -= R::f32(y[i]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float d = ok ? v[e] : 0.f;
+        sum = __builtin_fmaf(d, d, sum);
+      }
     }
   }
   red[tid] = sum;
