@@ -28,11 +28,21 @@ def r_quantile(values, r):
     return v[max(0, min(len(v) - 1, int(math.ceil(r * len(v))) - 1))]
 
 
-def run(steps: Sequence[Dict[str, np.ndarray]], offsets, q, g, R, eps_local, scale, force=None):
+def run(steps: Sequence[Dict[str, np.ndarray]], offsets, q, g, R, eps_local, scale, force=None,
+        evaluate=False):
     """``force`` (optional) maps a step t to a decision (anchor, groups to
     compute) taken instead of the rule's, after the rule's inputs (ASE,
     drift, eps) have been formed: a test re-synchronises with a run whose
-    decision differed on a near-tie."""
+    decision differed on a near-tie.
+
+    ``evaluate``: at every non-anchor step also record, for every group, the
+    error its cached state actually carries, the quantity ASE predicts
+    (Eq. ase_decomposition with the true state change instead of
+    Eq. error_extrapolation): w(G, t) ||AS_t(G) - AS_tc(G)||, with AS_t(G)
+    the group's state composed from fresh states of step t, AS_tc(G) its
+    cached state before the step's recomputation, and w(G, t) the sum of its
+    partitions' weights in the full composition at step t (Eq. lse_weight at
+    t).  Evaluation only: it costs a full attention pass per step."""
     P = len(offsets) - 1
     groups = groups_of(P, q, g)
     part = lambda qx, x, j: partition_state(qx, x["k"][:, offsets[j]:offsets[j + 1]],
@@ -44,7 +54,7 @@ def run(steps: Sequence[Dict[str, np.ndarray]], offsets, q, g, R, eps_local, sca
     for t, x in enumerate(steps):
         qx = x["q"][:, offsets[q]:offsets[q + 1]]
         local = part(qx, x, q)
-        ase, drift = {}, None
+        ase, drift, measured = {}, None, None
         if t_a is None:
             anchor = True
         else:
@@ -55,6 +65,15 @@ def run(steps: Sequence[Dict[str, np.ndarray]], offsets, q, g, R, eps_local, sca
             if eps is None:
                 eps = r_quantile(list(ase.values()), R)
             anchor = all(ase[grp] > eps for grp in groups) or drift > eps_local
+            if evaluate:
+                sts = [part(qx, x, j) for j in range(P)]
+                _, full_lse = merge([s_[0] for s_ in sts], [s_[1] for s_ in sts])
+                _, w_t = contrib([s_[1] for s_ in sts], full_lse)
+                measured = {}
+                for grp in groups:
+                    fresh_g = merge([sts[j][0] for j in range(*grp)], [sts[j][1] for j in range(*grp)])
+                    measured[grp] = (sum(w_t[j] for j in range(*grp)) *
+                                     float(np.linalg.norm(fresh_g[0] - cache[grp][0])))
         forced = force is not None and t in force
         if forced:
             anchor = bool(force[t][0])
@@ -90,5 +109,5 @@ def run(steps: Sequence[Dict[str, np.ndarray]], offsets, q, g, R, eps_local, sca
         out, lse = merge([cache[grp][0] for grp in groups] + [local[0]],
                          [cache[grp][1] for grp in groups] + [local[1]])
         results.append(dict(anchor=anchor, compute=compute, ase=ase, eps=eps, drift=drift, out=out, lse=lse,
-                            t_c=dict(t_c), corrections=list(corrections)))
+                            t_c=dict(t_c), corrections=list(corrections), measured=measured))
     return results

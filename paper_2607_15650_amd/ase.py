@@ -43,9 +43,28 @@ def quantile_r(values: Sequence[float], r: float) -> float:
     return float(v[k - 1])
 
 
+def accuracy_stats(predicted: Sequence[float], measured: Sequence[float]) -> Dict[str, float]:
+    """How well predicted errors match measured ones: R^2 of the prediction as
+    it stands (1 - sum (m - p)^2 / sum (m - mean m)^2, no fitted line),
+    Pearson's r, RMSE and MAE, over paired samples."""
+    p = np.asarray(predicted, dtype=np.float64)
+    m = np.asarray(measured, dtype=np.float64)
+    if p.size < 2:
+        return {"n": int(p.size), "r2": float("nan"), "pearson": float("nan"),
+                "rmse": float("nan"), "mae": float("nan")}
+    res = m - p
+    ss_tot = float(np.sum((m - m.mean()) ** 2))
+    r2 = 1.0 - float(np.sum(res ** 2)) / ss_tot if ss_tot > 0 else float("nan")
+    sp, sm = p.std(), m.std()
+    pearson = float(np.mean((p - p.mean()) * (m - m.mean())) / (sp * sm)) if sp > 0 and sm > 0 else float("nan")
+    return {"n": int(p.size), "r2": r2, "pearson": pearson, "rmse": float(np.sqrt(np.mean(res ** 2))),
+            "mae": float(np.mean(np.abs(res)))}
+
+
 class ErrorModelSelectiveAttention:
     def __init__(self, B: int, H: int, D: int, offsets: Sequence[int], q: int, g: int, scale: float,
-                 reuse_ratio: float, eps_local: float, dtype=torch.bfloat16, device="cuda"):
+                 reuse_ratio: float, eps_local: float, dtype=torch.bfloat16, device="cuda",
+                 evaluate: bool = False):
         self.B, self.H, self.D = B, H, D
         self.offsets = [int(o) for o in offsets]
         self.P = len(self.offsets) - 1
@@ -53,6 +72,9 @@ class ErrorModelSelectiveAttention:
         self.scale = float(scale)
         self.R, self.eps_local = float(reuse_ratio), float(eps_local)
         self.dtype, self.device = dtype, device
+        # evaluation of the error model (costs a full attention pass per
+        # step): record the error every cached group state actually carries
+        self.evaluate = bool(evaluate)
         self.L = self.offsets[q + 1] - self.offsets[q]
         shp = (self.P, B, self.L, H, D)
         self.cache = torch.zeros(shp, dtype=dtype, device=device)
@@ -99,7 +121,9 @@ class ErrorModelSelectiveAttention:
 
     # ---------------------------------------------------------------- one step
     def step(self, t: int, q_all: torch.Tensor, k: torch.Tensor, v: torch.Tensor):
-        """Returns (OUT, LSE, info) with info = dict(anchor, compute, ase, eps, drift)."""
+        """Returns (OUT, LSE, info) with info = dict(anchor, compute, ase, eps, drift), and,
+        when the model is evaluated, ``measured`` (group -> the error its cached
+        state actually carries) at every step after the first."""
         a, e = self.offsets[self.q], self.offsets[self.q + 1]
         qb = q_all[:, a:e].contiguous()
         loc = [0] * self.P
@@ -119,6 +143,8 @@ class ErrorModelSelectiveAttention:
                 self.eps = quantile_r(list(ase.values()), self.R)
             info.update(ase=ase, eps=self.eps, drift=drift)
             anchor = all(x > self.eps for x in ase.values()) or drift > self.eps_local
+            if self.evaluate:
+                info["measured"] = self._measure(qb, k, v)
         if anchor:
             compute = list(self.groups)
             self._anchor(t, qb, k, v)
@@ -142,6 +168,27 @@ class ErrorModelSelectiveAttention:
         api.merge_states(self.cache, self.cache_lse, out, lse, slots=slots)
         info.update(anchor=anchor, compute=compute)
         return out, lse, info
+
+    def _measure(self, qb, k, v) -> Dict[Tuple[int, int], float]:
+        """The error each cached group state carries at this step, the
+        quantity the ASE of Eq. ase_decomposition models: w(G, t) ||AS_t(G) -
+        AS_tc(G)||, with every partition computed fresh (evaluation only, in
+        the anchor buffers, which are free between anchors), each group's
+        fresh state composed, and w(G, t) its partitions' weights in the full
+        composition of this step (Eq. lse_weight at t)."""
+        self._attn(qb, k, v, [1] * self.P, self.fresh, self.fresh_lse)
+        out = torch.empty((self.B, self.L, self.H, self.D), dtype=self.dtype, device=self.device)
+        lse = torch.empty((self.B, self.H, self.L), dtype=torch.float32, device=self.device)
+        api.merge_states(self.fresh, self.fresh_lse, out, lse)
+        w = torch.empty(self.P, dtype=torch.float32, device=self.device)
+        api.contrib(self.fresh_lse, lse, w, self._ws)
+        w_t = w.cpu().tolist()
+        measured = {}
+        for grp in self.groups:
+            self._compose_group(self.fresh, self.fresh_lse, grp)
+            n = self._norms(self.fresh, [grp[0]], ref=self.cache[grp[0]])[0]
+            measured[grp] = sum(w_t[j] for j in range(*grp)) * n
+        return measured
 
     def _anchor(self, t: int, qb, k, v) -> None:
         sel = [1] * self.P

@@ -53,6 +53,8 @@
 //
 // Accumulator layout of the 32x32 MFMA (lane l, register r):
 //   row i = 8*(r/4) + 4*(l/32) + (r%4), column j = l % 32.
+#include <type_traits>
+
 #include "internal.h"
 
 
@@ -113,6 +115,15 @@ __device__ __forceinline__ float pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// f(std::integral_constant<int, I>{}) for I = 0 .. N-1, unrolled
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
+}
+
 template <int D, int QB, int NW, int BN, int NBUF>
 struct Cfg {
   static constexpr int NT = NW * 64;          // threads per workgroup
@@ -131,7 +142,11 @@ struct Cfg {
   // vmcnt(n): tile loads a wave may leave in flight at the end of an
   // iteration (those issued in the last PF-1 iterations)
   static constexpr int VM_LEFT = (PF - 1) * 2 * LOADS_W;
-  static_assert(NBUF >= 2 && (NBUF & (NBUF - 1)) == 0, "ring size");
+  // dynamic LDS: the K and V rings, one Q/OUT staging region per wave and
+  // the claimed unit of a queue workgroup
+  static constexpr size_t LDS_BYTES = (size_t)2 * NBUF * TILEB + (size_t)NW * QB * 32 * ROWB + 16;
+  static_assert(LDS_BYTES <= 163840, "LDS of one compute unit");
+  static_assert(NBUF >= 2 && NBUF <= 4, "ring size");   // the unrolled loop keeps slots constant
   static_assert(VM_LEFT <= 63, "vmcnt range");
   static_assert(D == 64 || D == 128, "head dim");
   static_assert(LOADS % NW == 0, "tile loads must split evenly over waves");
@@ -388,10 +403,10 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
 
   // rings of NBUF K tiles and NBUF V tiles (LDS byte addresses): tile t lives
   // in slot t % NBUF
-  auto kbuf_lds = [&](int t) { return smem_lds + (uint32_t)((t & (NBUF - 1)) * C::TILEB); };
-  auto vbuf_lds = [&](int t) { return smem_lds + (uint32_t)((NBUF + (t & (NBUF - 1))) * C::TILEB); };
-  auto kbuf = [&](int t) { return smem + (t & (NBUF - 1)) * C::TILEB; };
-  auto vbuf = [&](int t) { return smem + (NBUF + (t & (NBUF - 1))) * C::TILEB; };
+  auto kbuf_lds = [&](int t) { return smem_lds + (uint32_t)((t % NBUF) * C::TILEB); };
+  auto vbuf_lds = [&](int t) { return smem_lds + (uint32_t)((NBUF + t % NBUF) * C::TILEB); };
+  auto kbuf = [&](int t) { return smem + (t % NBUF) * C::TILEB; };
+  auto vbuf = [&](int t) { return smem + (NBUF + t % NBUF) * C::TILEB; };
 
   // K A-operand: lane reads unit (2s + g) of row kb*32 + lr
   const int krow_off = lr * C::ROWB;
@@ -530,16 +545,19 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   // of tile i.  Block A: the MFMAs of S_{i+1} = K_{i+1} Q^T run while the VALU
   // turns S_i into probabilities P_i (exp2, row sums, bf16).  Block B: the
   // MFMAs of O += V_i P_i.
-  auto iteration = [&](int i, f32x16 (&scur)[C::KB][QB], f32x16 (&snxt)[C::KB][QB]) {
-    const unsigned char* k_next = kbuf(i + 1);
-    const unsigned char* v_cur = vbuf(i);
+  // `ph` (a compile-time constant, i % NBUF) fixes every ring slot the
+  // iteration touches, so LDS addresses are constant offsets of one base.
+  auto iteration = [&](int i, auto ph, f32x16 (&scur)[C::KB][QB], f32x16 (&snxt)[C::KB][QB]) {
+    constexpr int P0 = decltype(ph)::value;
+    const unsigned char* k_next = smem + ((P0 + 1) % NBUF) * C::TILEB;
+    const unsigned char* v_cur = smem + (NBUF + P0) * C::TILEB;
     // Tile i is the partition's last and partial: mask its keys past the end.
     if ((i + 1) * BN > kv_len) mask_tail(scur, i * BN);
     // K_{i+1+PF} and V_{i+PF} land in LDS during the next PF iterations; they
     // overwrite K_{i+1+PF-NBUF} and V_{i+PF-NBUF}, consumed before the last
     // barrier
-    load_tile(kg, kbuf_lds(i + 1 + C::PF), (i + 1 + C::PF) * BN, true);
-    load_tile(vg, vbuf_lds(i + C::PF), (i + C::PF) * BN, false);
+    load_tile(kg, smem_lds + (uint32_t)(((P0 + 1 + C::PF) % NBUF) * C::TILEB), (i + 1 + C::PF) * BN, true);
+    load_tile(vg, smem_lds + (uint32_t)((NBUF + (P0 + C::PF) % NBUF) * C::TILEB), (i + C::PF) * BN, false);
     qk(k_next, snxt);
     bf16x8 pf[QB][C::PS];
     softmax_checked(scur, pf);
@@ -596,10 +614,20 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
       qk(kbuf(0), s0);
       // every wave has read K_0 before iteration 0 loads K_2 into its slot
       __syncthreads();
-      // K_i is consumed one iteration early (scores of the next tile)
-      for (int i = 0; i < n_tiles; i += 2) {
-        iteration(i, s0, s1);
-        if (i + 1 < n_tiles) iteration(i + 1, s1, s0);
+      // K_i is consumed one iteration early (scores of the next tile).  The
+      // loop is unrolled over U tiles, a multiple of both the ring size and
+      // the two score buffers, so that every ring slot is a constant.
+      constexpr int U = NBUF % 2 == 0 ? NBUF : 2 * NBUF;
+      for (int i = 0; i < n_tiles; i += U) {
+        static_for<U>([&](auto u) {
+          constexpr int k = decltype(u)::value;
+          if (k == 0 || i + k < n_tiles) {
+            if constexpr (k % 2 == 0)
+              iteration(i + k, std::integral_constant<int, k % NBUF>{}, s0, s1);
+            else
+              iteration(i + k, std::integral_constant<int, k % NBUF>{}, s1, s0);
+          }
+        });
       }
     }
   }
@@ -776,7 +804,7 @@ hipError_t set_lds(size_t lds) {
 template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
 hipError_t plan_cfg(const AttnArgs& a, Plan* p) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
-  const size_t lds = (size_t)2 * NBUF * C::TILEB + (size_t)NW * QB * 32 * C::ROWB + 16;
+  const size_t lds = C::LDS_BYTES;
   hipError_t e = set_lds<D, QB, NW, BN, NBUF, WPE, SEQ, TS>(lds);
   if (e != hipSuccess) return e;
   *p = Plan{};
@@ -806,7 +834,7 @@ hipError_t plan_cfg(const AttnArgs& a, Plan* p) {
 template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
 hipError_t launch_cfg(const AttnArgs& a0, void* ws, size_t ws_bytes, hipStream_t s) {
   using C = Cfg<D, QB, NW, BN, NBUF>;
-  const size_t lds = (size_t)2 * NBUF * C::TILEB + (size_t)NW * QB * 32 * C::ROWB + 16;
+  const size_t lds = C::LDS_BYTES;
   Plan p;
   const bool queued = ws != nullptr && ws_bytes >= kQueueBytes;
   if (queued) {

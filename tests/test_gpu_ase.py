@@ -97,3 +97,60 @@ def differing_margin(o, ga, gc):
         return min(abs(c_ase), abs(c_drift))
     diff = set(gc) ^ set(o["compute"])
     return max(abs(o["ase"][grp] - o["eps"]) / eps for grp in diff)
+
+
+def test_error_model_accuracy_against_oracle_reduced():
+    """The error model's evaluation (Sec. 4.1.2; the paper's accuracy study
+    of Sec. 6.5 repeated on synthetic tensors): at every step after the first,
+    each group's predicted ASE and the error its cached state actually
+    carries, w(G, t) ||AS_t(G) - AS_tc(G)||, on the GPU against the float64
+    oracle, and the R^2 / Pearson of prediction against measurement on both
+    sides.  The oracle follows the GPU's decisions where they differ on a
+    near-tie, as in the test above."""
+    import torch
+    from paper_2607_15650_amd.ase import ErrorModelSelectiveAttention, accuracy_stats
+
+    w = get_workload("planner_bf16_h2_d128_s16384_p8_10steps")
+    x = gen_qkv(w, with_prev=False)
+    steps = [x]
+    for s in range(w.steps - 1):
+        steps.append(gen_evolved(w, steps[-1], s))
+    offs = w.offsets
+    X = [{n: exact_inputs(v_, "bf16") for n, v_ in xs.items()} for xs in steps]
+    pairs_g, pairs_o = [], []
+    worst = {"ase": 0.0, "measured": 0.0}
+    for qb in (3, 6):
+        em = ErrorModelSelectiveAttention(w.B, w.H, w.D, offs, qb, G, w.scale, R, EPS_LOCAL, torch.bfloat16,
+                                          evaluate=True)
+        gpu = []
+        for t, xs in enumerate(steps):
+            q, k, v = (to_gpu(xs[n], "bf16") for n in ("q", "k", "v"))
+            _, _, info = em.step(t, q, k, v)
+            gpu.append(info)
+        force = {}
+        orc = ase_planner.run(X, offs, qb, G, R, EPS_LOCAL, w.scale, evaluate=True)
+        t = 1
+        while t < w.steps:
+            gi, o = gpu[t], orc[t]
+            for key in ("ase", "measured"):
+                for grp, gv in gi[key].items():
+                    ov = o[key][grp]
+                    rel = abs(gv - ov) / max(abs(ov), 1e-30)
+                    worst[key] = max(worst[key], rel)
+                    assert rel <= 0.03, (qb, t, key, grp, gv, ov)
+            if (gi["anchor"], list(gi["compute"])) != (o["anchor"], o["compute"]):
+                m = differing_margin(o, gi["anchor"], list(gi["compute"]))
+                assert m <= 0.02, (qb, t, m)
+                force[t] = (gi["anchor"], list(gi["compute"]))
+                orc = ase_planner.run(X, offs, qb, G, R, EPS_LOCAL, w.scale, force=force, evaluate=True)
+                continue
+            for grp in gi["ase"]:
+                pairs_g.append((gi["ase"][grp], gi["measured"][grp]))
+                pairs_o.append((o["ase"][grp], o["measured"][grp]))
+            t += 1
+    sg = accuracy_stats(*zip(*pairs_g))
+    so = accuracy_stats(*zip(*pairs_o))
+    print(f"error model (synthetic, reduced shape): GPU {sg}  oracle {so}  "
+          f"worst relative difference {worst}", flush=True)
+    assert sg["n"] == so["n"] >= 30
+    assert abs(sg["r2"] - so["r2"]) <= 0.02 and abs(sg["pearson"] - so["pearson"]) <= 0.01

@@ -174,6 +174,7 @@ def test_error_planner_closed_forms_under_a_value_scaling(c):
 #   ASE_t(G)        = |c_t - c_{t_c(G)}| A_G           (local snapshot at t_c)
 #   relative drift  = |c_t - c_{t_a}| / (1 + c_{t_a})
 #   correction(G)   = |c_t - c_{t_c(G)}| B_G           (at an anchor t)
+#   measured error  = |c_t - c_{t_c(G)}| B_G           (any step t > t_a)
 #   composed LSE    = the full-attention LSE at every step.
 # The step-0 quantities come from torch's float64 attention and scipy's
 # logsumexp over each partition's and group's key range, not from the oracle.
@@ -200,7 +201,7 @@ def test_error_planner_eps_adaptation_over_several_anchors():
     x0 = seq(7)
     c = [0.0, 0.05, 0.08, 0.3, 0.32, 0.6, 0.62]
     xs = [dict(x0, v=x0["v"] * (1.0 + ct)) for ct in c]
-    res = ase_planner.run(xs, offs, q, g, R, eps_local, scale)
+    res = ase_planner.run(xs, offs, q, g, R, eps_local, scale, evaluate=True)
 
     out_of, lse_of = _truth_by_key_range(x0, offs, q, scale)
     lse_full = lse_of(0, S)
@@ -220,6 +221,9 @@ def test_error_planner_eps_adaptation_over_several_anchors():
     for t in range(1, len(c)):
         r = res[t]
         ase = {G: abs(c[t] - c[t_c[G]]) * A[G] for G in groups}
+        # the error each cached group state actually carries (evaluation)
+        for G in groups:
+            assert r["measured"][G] == pytest.approx(abs(c[t] - c[t_c[G]]) * Bc[G], rel=1e-9, abs=1e-15), (t, G)
         drift = abs(c[t] - c[t_a]) / (1.0 + c[t_a])
         assert r["drift"] == pytest.approx(drift, rel=1e-9, abs=1e-15)
         for G in groups:
@@ -251,3 +255,43 @@ def test_error_planner_eps_adaptation_over_several_anchors():
     assert sorted(set(res[2]["t_c"].values())) == [0, 1, 2]
     assert len(res[5]["corrections"]) == 8 and len(res[4]["corrections"]) == 4
     assert res[5]["eps"] == pytest.approx(sorted(res[5]["corrections"])[3], rel=0)
+
+
+def test_error_planner_measured_errors_by_key_range_on_changing_tensors():
+    """Tensors that change at every step (LSEs and weights move): the
+    measured error of a group, w(G, t) ||AS_t(G) - AS_tc(G)||, recomputed
+    from torch's float64 attention over the group's key range at steps t and
+    t_c (a group's composed state is attention over the union of its keys)
+    and scipy's logsumexp for the current weight."""
+    from scipy.special import logsumexp
+    torch = pytest.importorskip("torch")
+    S, P, q, scale, g = 48, 8, 3, 0.35, 2
+    offs = partition_offsets(S, P)
+    xs = [seq(30 + s, S=S) for s in range(5)]
+    res = ase_planner.run(xs, offs, q, g, 0.5, 10.0, scale, evaluate=True)
+    groups = og.groups_of(P, q, g)
+
+    def attn(x, a, e):
+        t = lambda y: torch.from_numpy(np.ascontiguousarray(y)).permute(0, 2, 1, 3)
+        Q = x["q"][:, offs[q]:offs[q + 1]]
+        o = torch.nn.functional.scaled_dot_product_attention(t(Q), t(x["k"][:, a:e]), t(x["v"][:, a:e]), scale=scale)
+        return o.permute(0, 2, 1, 3).numpy()
+
+    def lse(x, a, e):
+        Q = x["q"][:, offs[q]:offs[q + 1]]
+        return logsumexp(scale * np.einsum("brhd,bchd->bhrc", Q, x["k"][:, a:e]), axis=-1)
+
+    checked = 0
+    for t in range(1, len(xs)):
+        r = res[t]
+        t_c = res[t - 1]["t_c"]                 # before this step's recomputation
+        assert r["measured"] is not None
+        for G in groups:
+            a, e = offs[G[0]], offs[G[1]]
+            w = float(np.mean(np.exp(lse(xs[t], a, e) - lse(xs[t], 0, S))))
+            expect = w * float(np.linalg.norm(attn(xs[t], a, e) - attn(xs[t_c[G]], a, e)))
+            assert r["measured"][G] == pytest.approx(expect, rel=1e-9), (t, G)
+            checked += 1
+    assert res[0]["measured"] is None and checked == 4 * len(groups)
+    # groups were recomputed between steps, so several cache ages were seen
+    assert len({tc for t in range(len(xs)) for tc in res[t]["t_c"].values()}) > 2

@@ -95,3 +95,17 @@ def test_product_quantile_hand_examples():
     assert quantile_r(v, 0.51) == 3.0
     assert quantile_r(v, 1.0) == 4.0
     assert quantile_r([0.3, 0.1, 0.2, 0.9, 0.5, 0.7, 0.8, 0.6], 0.5) == 0.5   # 4th of 8
+
+
+def test_accuracy_stats_hand_examples():
+    from paper_2607_15650_amd.ase import accuracy_stats
+    st = accuracy_stats([1.0, 2.0, 3.0], [1.0, 2.0, 3.0])
+    assert st["r2"] == 1.0 and abs(st["pearson"] - 1.0) < 1e-15 and st["rmse"] == 0.0 and st["mae"] == 0.0
+    # prediction off by a constant 1: r = 1, R^2 = 1 - 3/2, RMSE = MAE = 1
+    st = accuracy_stats([2.0, 3.0, 4.0], [1.0, 2.0, 3.0])
+    assert abs(st["pearson"] - 1.0) < 1e-15 and st["r2"] == -0.5 and st["rmse"] == 1.0 and st["mae"] == 1.0
+    # anti-correlated: r = -1
+    st = accuracy_stats([3.0, 2.0, 1.0], [1.0, 2.0, 3.0])
+    assert abs(st["pearson"] + 1.0) < 1e-15 and st["r2"] == 1.0 - 8.0 / 2.0
+    st = accuracy_stats([0.0, 1.0], [1.0, 0.0])
+    assert st["n"] == 2 and st["mae"] == 1.0
