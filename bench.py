@@ -38,11 +38,11 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # elementwise copy reads / writes 1 GiB), keyed by the build id (source and
 # compile options) of the kernel they were taken on; reported only while the
 # build id matches.
-ATTN_TRAFFIC = {"build_id": "4c653360a1b0abf3", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "queue",
+ATTN_TRAFFIC = {"build_id": "31d9b98986c5dac1", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "queue",
                 # the balanced attention kernel (mean of 5 launches: the order
                 # in which tasks are claimed moves the reads by up to 1 %); the
                 # counter reset moves about 1 KiB
-                "fetch_bytes": 761559 * 1024 * 2.0, "write_bytes": 287961 * 1024 * 1.0}
+                "fetch_bytes": 762545.16 * 1024 * 2.0, "write_bytes": 287971.86 * 1024 * 1.0}
 
 
 def parse():
@@ -99,14 +99,14 @@ def algorithmic(w, select):
 # rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_LDS_BANK_CONFLICT
 # (busy fraction = busy cycles / (1024 SIMDs x GRBM cycles / 8 XCDs); clock =
 # GRBM cycles / 8 / the traced kernel duration); reported under the same rule.
-ATTN_COUNTERS = {"mfma_busy": 0.631, "lds_bank_conflicts": 2269440, "clock_ghz": 1.81}
+ATTN_COUNTERS = {"mfma_busy": 0.636, "lds_bank_conflicts": 2269440, "clock_ghz": 1.83}
 
 
 # HBM bytes per launch of the merge kernel at the default workload (all P
 # slots), from the same two counter runs and scaled the same way; reported
 # only while merge.hip's build id matches.
-MERGE_TRAFFIC = {"build_id": "e68c09e2a7a5fd5e", "workload": "videodit_bf16_h40_d128_s75600_p8",
-                 "fetch_bytes": 401743.5 * 1024 * 2.0, "write_bytes": 100409 * 1024 * 1.0}
+MERGE_TRAFFIC = {"build_id": "b8d356210acd6f42", "workload": "videodit_bf16_h40_d128_s75600_p8",
+                 "fetch_bytes": 401726.0 * 1024 * 2.0, "write_bytes": 100415.0 * 1024 * 1.0}
 
 
 def merge_traffic(w):
