@@ -29,6 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "selective-attn step time (ms) + effective TFLOP/s and % bf16 MFMA peak, 1 GPU"
+DEFAULT_WORKLOAD = "videodit_bf16_h40_d128_s75600_p8"
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3        # MI355X fp32 MFMA / vector
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
@@ -50,7 +51,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="videodit_bf16_h40_d128_s75600_p8")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--select", default=None, help="comma-separated fresh partitions (default: the workload's)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time of the oracle baseline sample (0 disables it)")
@@ -77,6 +78,9 @@ def parse():
                     help="skip the step-time-against-selected-fraction points")
     ap.add_argument("--power-seconds", type=float, default=3.0,
                     help="sample socket power and clocks for this long per kernel after timing (0 disables)")
+    ap.add_argument("--no-other-workloads", dest="other_workloads", action="store_false",
+                    help="default workload: skip the long-context sweep and the planner-driven run that "
+                         "the line also carries")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before timing, run one plain elementwise copy of this many MiB "
                          "(the reference kernel that scales profiler byte counters)")
@@ -307,70 +311,96 @@ def power_during(torch, fn, seconds=3.0):
             "gfx_mhz_min": min(clocks), "gfx_mhz_max": max(clocks), "samples": len(use)}
 
 
-def multistep(args, w):
-    """Planner-driven run: every query block, w.steps denoising steps, anchors
-    compute every partition, other steps the query partition plus every
-    partition whose anchor weight exceeds w.threshold.  Reports the selective
-    attention time, the all-fresh time and the drift of the selective output
-    from fresh full attention at every step."""
+def planner_result(w, thresholds):
+    """Planner-driven run: every query block, w.steps denoising steps; for
+    each threshold, anchors compute every partition and other steps the query
+    partition plus every partition whose anchor weight exceeds it.  One set of
+    evolving inputs serves every threshold and the all-fresh reference.
+    Returns, per threshold, the selective attention time, the all-fresh time
+    and the drift of the selective output from fresh full attention."""
     import numpy as np
     import torch
     from fixtures import bf16_bits, gen_qkv, gen_evolved
-    from paper_2607_15650_amd import api
     from paper_2607_15650_amd.planner import AnchorPlanner
     from paper_2607_15650_amd.step import SelectiveAttention
 
     offs = w.offsets
     blocks = list(range(w.P))
     g = lambda a: torch.from_numpy(bf16_bits(a).view(np.int16)).view(torch.bfloat16).cuda()
-    sa = SelectiveAttention(w.B, w.H, w.D, offs, w.scale, torch.bfloat16)
+    runs = {thr: {"sa": SelectiveAttention(w.B, w.H, w.D, offs, w.scale, torch.bfloat16),
+                  "pl": {qb: AnchorPlanner(w.P, qb, w.anchors, thr) for qb in blocks},
+                  "t": 0.0, "flops": 0.0, "per_step": []} for thr in thresholds}
     ref = SelectiveAttention(w.B, w.H, w.D, offs, w.scale, torch.bfloat16)
-    planners = {qb: AnchorPlanner(w.P, qb, w.anchors, w.threshold) for qb in blocks}
     x = gen_qkv(w, with_prev=False)
     ev = lambda: torch.cuda.Event(enable_timing=True)
-    t_sel = t_full = 0.0
-    flops_sel = flops_full = 0.0
-    per_step = []
+    t_full = flops_full = 0.0
     for s in range(w.steps):
         q, k, v = g(x["q"]), g(x["k"]), g(x["v"])
         torch.cuda.synchronize()
-        masks, drift, maxabs = [], [], []
+        fresh = {}
         for qb in blocks:
-            mask = planners[qb].select(s)
-            L = offs[qb + 1] - offs[qb]
-            e0, e1, e2 = ev(), ev(), ev()
+            e0, e1 = ev(), ev()
             e0.record()
-            out, lse, wp = sa.step(s, qb, q, k, v, mask)
+            fo, _, _ = ref.step(s, qb, q, k, v, [1] * w.P)
             e1.record()
-            fo, fl, _ = ref.step(s, qb, q, k, v, [1] * w.P)
-            e2.record()
             torch.cuda.synchronize()
-            t_sel += e0.elapsed_time(e1)
-            t_full += e1.elapsed_time(e2)
-            keys = sum(offs[j + 1] - offs[j] for j in range(w.P) if mask[j])
-            flops_sel += 4.0 * w.B * w.H * L * w.D * keys
+            t_full += e0.elapsed_time(e1)
+            L = offs[qb + 1] - offs[qb]
             flops_full += 4.0 * w.B * w.H * L * w.D * offs[-1]
-            planners[qb].observe(s, wp.cpu().numpy())
-            d = (out.float() - fo.float())
-            drift.append(float(d.norm() / fo.float().norm()))
-            maxabs.append(float(d.abs().max()))
-            masks.append("".join(str(m) for m in mask))
-        per_step.append({"step": s, "anchor": s in w.anchors, "masks": masks,
-                         "drift_rel_l2_max": max(drift), "drift_maxabs_max": max(maxabs)})
-        print(f"[bench] step {s} masks {masks} drift {max(drift):.3e}", file=sys.stderr, flush=True)
+            fresh[qb] = fo.float()
+        for thr, r in runs.items():
+            masks, drift, maxabs = [], [], []
+            for qb in blocks:
+                mask = r["pl"][qb].select(s)
+                L = offs[qb + 1] - offs[qb]
+                e0, e1 = ev(), ev()
+                e0.record()
+                out, _, wp = r["sa"].step(s, qb, q, k, v, mask)
+                e1.record()
+                torch.cuda.synchronize()
+                r["t"] += e0.elapsed_time(e1)
+                keys = sum(offs[j + 1] - offs[j] for j in range(w.P) if mask[j])
+                r["flops"] += 4.0 * w.B * w.H * L * w.D * keys
+                r["pl"][qb].observe(s, wp.cpu().numpy())
+                d = out.float() - fresh[qb]
+                drift.append(float(d.norm() / fresh[qb].norm()))
+                maxabs.append(float(d.abs().max()))
+                masks.append("".join(str(m) for m in mask))
+            r["per_step"].append({"step": s, "anchor": s in w.anchors, "masks": masks,
+                                  "drift_rel_l2_max": max(drift), "drift_maxabs_max": max(maxabs)})
+            print(f"[bench] {w.name} thr {thr} step {s} masks {masks} drift {max(drift):.3e}",
+                  file=sys.stderr, flush=True)
+        del fresh
         if s + 1 < w.steps:
             x = gen_evolved(w, x, s)
+    out = {}
+    for thr, r in runs.items():
+        out[str(thr)] = {"threshold": thr, "selective_ms_per_step": r["t"] / w.steps,
+                         "all_fresh_ms_per_step": t_full / w.steps, "speedup_vs_all_fresh": t_full / r["t"],
+                         "computed_fraction": r["flops"] / flops_full,
+                         "tflops_selective": r["flops"] / (r["t"] * 1e-3) / 1e12, "per_step": r["per_step"]}
+    return {"workload": w.name, "steps": w.steps, "query_blocks": len(blocks), "anchors": list(w.anchors),
+            "by_threshold": out,
+            "note": "times are the calls of each block's step on the stream (attention, composition, "
+                    "weights); each block's step is synchronised to read its weights back for the planner"}
+
+
+def multistep(args, w):
+    """Planner-driven run at one threshold (the workload's or --threshold)."""
+    thr = w.threshold
+    r = planner_result(w, [thr])
+    t = r["by_threshold"][str(thr)]
     res = {
-        "metric": METRIC, "value": flops_sel / (t_sel * 1e-3) / 1e12, "unit": "TFLOP/s", "n_gpus": 1,
-        "steps": w.steps, "warmup": 0, "ms_per_step": t_sel / w.steps, "higher_is_better": True,
+        "metric": METRIC, "value": t["tflops_selective"], "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": w.steps, "warmup": 0, "ms_per_step": t["selective_ms_per_step"], "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
         "data": "synthetic (seeded; each step adds 0.03*N(0,1) to Q, K, V)",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "D": w.D, "S": w.S, "P": w.P,
-                   "query_blocks": len(blocks), "anchors": list(w.anchors), "threshold": w.threshold},
-        "selective_ms_total": t_sel, "all_fresh_ms_total": t_full, "speedup_vs_all_fresh": t_full / t_sel,
-        "computed_fraction": flops_sel / flops_full, "per_step": per_step,
-        "note": "times include every call's launch on the stream; each block's step is synchronised "
-                "to read its weights back for the planner",
+                   "query_blocks": r["query_blocks"], "anchors": r["anchors"], "threshold": thr},
+        "selective_ms_total": t["selective_ms_per_step"] * w.steps,
+        "all_fresh_ms_total": t["all_fresh_ms_per_step"] * w.steps,
+        "speedup_vs_all_fresh": t["speedup_vs_all_fresh"], "computed_fraction": t["computed_fraction"],
+        "per_step": t["per_step"], "note": r["note"],
     }
     print(json.dumps(res), flush=True)
 
@@ -443,8 +473,10 @@ def multistep_error_model(args, w):
     print(json.dumps(res), flush=True)
 
 
-def sweep(args, w):
-    """Step time for each selection of the workload's sweep (nearest-first sizes)."""
+def sweep_result(w, steps, warmup):
+    """Step time for each selection of the workload's sweep (nearest-first
+    sizes), the other partitions' states read from the cache, and the line
+    through step time against the selected fraction."""
     import numpy as np
     import torch
     from fixtures import bf16_bits, gen_qkv
@@ -465,6 +497,7 @@ def sweep(args, w):
     wp = torch.empty(w.P, dtype=torch.float32, device="cuda")
     ws = torch.empty(max(16, api.contrib_workspace_bytes(w.B, w.H, L, w.P)), dtype=torch.uint8, device="cuda")
     api.attn_partition_states(qp, kp, vp, offs, [1] * w.P, w.scale, st, ls)
+    del qp, kp, vp
     rows = []
     for sel in w.sweep:
         mask = [1 if j in sel else 0 for j in range(w.P)]
@@ -475,31 +508,37 @@ def sweep(args, w):
             api.attn_partition_states(q, k, v, offs, mask, w.scale, st, ls, ws_k)
             api.merge_states(st, ls, out, lse)
             api.contrib(ls, lse, wp, ws)
-        for _ in range(args.warmup):
+        for _ in range(warmup):
             step()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record()
-        for _ in range(args.steps):
+        for _ in range(steps):
             step()
         e1.record()
         torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / args.steps
+        ms = e0.elapsed_time(e1) / steps
         flops = algorithmic(w, sel)[0]
         rows.append({"k": len(sel), "fraction": len(sel) / w.P, "ms_per_step": ms,
                      "tflops": flops / (ms * 1e-3) / 1e12})
-        print(f"[bench] k={len(sel)} {ms:.3f} ms", file=sys.stderr, flush=True)
+        print(f"[bench] {w.name} k={len(sel)} {ms:.3f} ms", file=sys.stderr, flush=True)
     ks = np.array([r["fraction"] for r in rows])
     ts = np.array([r["ms_per_step"] for r in rows])
     slope, icpt = np.polyfit(ks, ts, 1)
-    full = rows[-1]
+    return {"workload": w.name, "steps": steps, "warmup": warmup, "points": rows,
+            "linear_fit_ms": {"slope_per_fraction": float(slope), "intercept": float(icpt)}}
+
+
+def sweep(args, w):
+    r = sweep_result(w, args.steps, args.warmup)
+    full = r["points"][-1]
     res = {
         "metric": METRIC, "value": full["tflops"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": full["ms_per_step"], "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "D": w.D, "S": w.S, "P": w.P,
-                   "query_partition": w.q, "q_len": L},
-        "sweep": rows, "linear_fit_ms": {"slope_per_fraction": slope, "intercept": icpt},
+                   "query_partition": w.q, "q_len": w.q_len},
+        "sweep": r["points"], "linear_fit_ms": r["linear_fit_ms"],
     }
     print(json.dumps(res), flush=True)
 
@@ -758,7 +797,40 @@ def main():
         "cpu_baseline": cpu,
         "input_gen_s": t_gen,
     }
+    if args.other_workloads and args.workload == DEFAULT_WORKLOAD:
+        res["other_workloads"] = other_workloads()
     print(json.dumps(res), flush=True)
+
+
+def other_workloads():
+    """The other workloads of the hot path, measured in the same run: the
+    long-context selection sweep (131,072 tokens, 24 heads, 16 partitions,
+    nearest-first fresh sets of 1, 2, 4, 8 and 16 partitions) and the
+    planner-driven run (75,600 tokens, 40 heads, all 8 query blocks over 10
+    steps, anchors at steps 0 and 5) at the specified weight threshold 0.05
+    and at the uniform level 1/8.  Reported beside the headline figure, not in
+    it."""
+    import gc
+    import torch
+    from fixtures import get_workload
+    out = {}
+    t0 = time.perf_counter()
+    gc.collect()
+    torch.cuda.empty_cache()
+    print("[bench] other workloads: long-context sweep", file=sys.stderr, flush=True)
+    out["longctx_sweep"] = sweep_result(get_workload("longctx_bf16_h24_d128_s131072_p16"), steps=5, warmup=2)
+    gc.collect()
+    torch.cuda.empty_cache()
+    print("[bench] other workloads: planner-driven run", file=sys.stderr, flush=True)
+    r = planner_result(get_workload("planner_bf16_h40_d128_s75600_p8_10steps"), [0.05, 0.125])
+    for t in r["by_threshold"].values():
+        # the per-step masks of 8 blocks x 10 steps stay in the planner mode's own line
+        t["drift_rel_l2_max_by_step"] = [p["drift_rel_l2_max"] for p in t.pop("per_step")]
+    out["planner"] = r
+    gc.collect()
+    torch.cuda.empty_cache()
+    out["wall_s"] = time.perf_counter() - t0
+    return out
 
 
 if __name__ == "__main__":
