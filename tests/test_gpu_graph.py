@@ -76,3 +76,60 @@ def test_step_graph_replays_match_eager():
         torch.cuda.synchronize()
         for name, t, r in zip(("states", "lses", "out", "lse", "w_part"), (states, lses, out, lse, w_part), ref):
             assert torch.equal(t.view(torch.uint8), r.view(torch.uint8)), (rep, name)
+
+
+def test_allocation_free_step_graph_replays_match_eager():
+    """The step with nothing allocated by the library: the static attention
+    launch (no workspace), the composition and ditango_contrib_noalloc (the
+    weights' partial sums in the library's fixed device array), captured as
+    a graph.  Between replays an eager call of the same entry point on other
+    sizes overwrites that array; every replay must still equal the eager step
+    bit for bit (each call writes every partial sum it reads)."""
+    import torch
+    a = api()
+    D, H, B = 128, 4, 1
+    lens = [500, 700, 300]
+    offs = [0]
+    for n in lens:
+        offs.append(offs[-1] + n)
+    P, S = len(lens), offs[-1]
+    q_len = 613
+    rng = np.random.default_rng(12)
+    q = to_gpu(rng.standard_normal((B, q_len, H, D), dtype=np.float32), "bf16")
+    k = to_gpu(rng.standard_normal((B, S, H, D), dtype=np.float32), "bf16")
+    v = to_gpu(rng.standard_normal((B, S, H, D), dtype=np.float32), "bf16")
+    scale = D ** -0.5
+    states = torch.zeros((P, B, q_len, H, D), dtype=torch.bfloat16, device="cuda")
+    lses = torch.zeros((P, B, H, q_len), dtype=torch.float32, device="cuda")
+    a.attn_partition_states(q, k, v, offs, [1] * P, scale, states, lses)
+    out = torch.empty((B, q_len, H, D), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((B, H, q_len), dtype=torch.float32, device="cuda")
+    w_part = torch.empty(P, dtype=torch.float32, device="cuda")
+    w_rows = torch.empty((B, H, q_len, P), dtype=torch.float32, device="cuda")
+    # other sizes, for eager calls between the replays
+    o_l = torch.randn((5, 2, 3, 2000), device="cuda")
+    o_lse = torch.logsumexp(o_l, dim=0)
+    o_wp = torch.empty(5, dtype=torch.float32, device="cuda")
+
+    def step():
+        a.attn_partition_states(q, k, v, offs, [1, 0, 1], scale, states, lses)
+        a.merge_states(states, lses, out, lse)
+        a.contrib_noalloc(lses, lse, w_part, w_rows)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (states, lses, out, lse, w_part, w_rows)]
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    for rep in range(4):
+        a.contrib_noalloc(o_l, o_lse, o_wp)
+        torch.cuda.synchronize()
+        for t in (out, lse, w_part, w_rows):
+            t.fill_(7.0)
+        graph.replay()
+        torch.cuda.synchronize()
+        for name, t, r in zip(("states", "lses", "out", "lse", "w_part", "w_rows"),
+                              (states, lses, out, lse, w_part, w_rows), ref):
+            assert torch.equal(t.view(torch.uint8), r.view(torch.uint8)), (rep, name)
