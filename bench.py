@@ -152,10 +152,18 @@ def attn_traffic(w, select, mode):
 
 def cpu_baseline(w, x, select, target_s):
     """The float64 oracle, as it stands, on a bounded sample of query rows of
-    the same step; scaled to the whole step by the row fraction."""
+    the same step; scaled to the whole step by the row fraction.  The heads
+    are independent in every oracle function, so the fresh states run one
+    head per task in a pool of len(os.sched_getaffinity(0)) threads (NumPy's
+    matrix products and exponentials release the interpreter lock), each
+    with single-threaded BLAS; the composition and the weights then run over
+    all heads at once.  Returns (rows, seconds, seconds per whole step,
+    workers)."""
+    import concurrent.futures as cf
     import numpy as np
     import oracle
     from fixtures import bf16_round
+    from threadpoolctl import threadpool_limits
     offs = w.offsets
     qa, qb = offs[w.q], offs[w.q + 1]
     cvt = (lambda a: bf16_round(a).astype(np.float64)) if w.dtype == "bf16" else (lambda a: a.astype(np.float64))
@@ -165,38 +173,39 @@ def cpu_baseline(w, x, select, target_s):
     Qall = cvt(x["q"][:, qa:qb])
     Qp_all = cvt(x["q_prev"][:, qa:qb]) if "q_prev" in x else Qall
     rng = np.random.default_rng(w.seed + 99)
+    workers = max(1, min(len(os.sched_getaffinity(0)), w.H * w.B))
+    sel = [j for j in range(w.P) if j in select]
 
-    def one(n):
+    def states(Q, Kx, Vx, parts, pool):
+        """oracle.partition_state of every partition in `parts`, one head per task."""
+        def head(h):
+            return [oracle.partition_state(Q[:, :, h:h + 1], Kx[:, offs[j]:offs[j + 1], h:h + 1],
+                                           Vx[:, offs[j]:offs[j + 1], h:h + 1], w.scale) for j in parts]
+        res = list(pool.map(head, range(w.H)))
+        return {j: (np.concatenate([r[i][0] for r in res], axis=2), np.concatenate([r[i][1] for r in res], axis=1))
+                for i, j in enumerate(parts)}
+
+    def one(n, pool):
         rows = np.sort(rng.choice(w.q_len, size=n, replace=False))
         Q = Qall[:, rows]
         Qp = Qp_all[:, rows]
         # cached states of the unselected partitions: filled before timing
-        cached = {j: oracle.partition_state(Qp, Kp[:, offs[j]:offs[j + 1]], Vp[:, offs[j]:offs[j + 1]], w.scale)
-                  for j in range(w.P) if j not in select}
+        cached = states(Qp, Kp, Vp, [j for j in range(w.P) if j not in select], pool)
         t0 = time.perf_counter()
-        outs, lses = [], []
-        for j in range(w.P):
-            if j in select:
-                o, l = oracle.partition_state(Q, K[:, offs[j]:offs[j + 1]], V[:, offs[j]:offs[j + 1]], w.scale)
-            else:
-                o, l = cached[j]
-            outs.append(o)
-            lses.append(l)
+        fresh = states(Q, K, V, sel, pool)
+        outs = [fresh[j][0] if j in fresh else cached[j][0] for j in range(w.P)]
+        lses = [fresh[j][1] if j in fresh else cached[j][1] for j in range(w.P)]
         out, lse = oracle.merge(outs, lses)
         oracle.contrib(lses, lse)
         return time.perf_counter() - t0
 
-    n0 = min(w.q_len, 32)
-    t0 = one(n0)
-    n = int(min(w.q_len, max(n0, n0 * target_s / max(t0, 1e-3))))
-    t = one(n) if n > n0 else t0
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:   # pragma: no cover
-        cores = 1
+    with threadpool_limits(1), cf.ThreadPoolExecutor(workers) as pool:
+        n0 = min(w.q_len, 32)
+        t0 = one(n0, pool)
+        n = int(min(w.q_len, max(n0, n0 * target_s / max(t0, 1e-3))))
+        t = one(n, pool) if n > n0 else t0
     per_step_s = t * w.q_len / n
-    return n, t, per_step_s, cores
+    return n, t, per_step_s, workers
 
 
 def cpu_description():
@@ -756,7 +765,9 @@ def main():
         n, t, per_step, cores = cpu_baseline(w, x, select, args.cpu_seconds)
         cpu = {"value": flops / per_step / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
                "sample": f"{n} of {q_len} query rows (all {w.H} heads, all keys of the fresh partitions), "
-                         f"{t:.2f} s; scaled by {q_len}/{n} to {per_step:.1f} s per step"}
+                         f"{t:.2f} s; scaled by {q_len}/{n} to {per_step:.1f} s per step",
+               "parallelism": f"fresh states one head per task on {cores} threads, single-threaded BLAS each; "
+                              "composition and weights over all heads in one thread"}
         cpu.update(cpu_description())
 
     res = {
