@@ -370,7 +370,13 @@ def planner_result(w, thresholds):
                 r["t"] += e0.elapsed_time(e1)
                 keys = sum(offs[j + 1] - offs[j] for j in range(w.P) if mask[j])
                 r["flops"] += 4.0 * w.B * w.H * L * w.D * keys
-                r["pl"][qb].observe(s, wp.cpu().numpy())
+                wp_h = wp.cpu().numpy()
+                r["pl"][qb].observe(s, wp_h)
+                if r["pl"][qb].is_anchor(s):
+                    # how far the anchor weights sit from the threshold (the
+                    # query partition is selected whatever its weight)
+                    m = min(abs(float(wp_h[j]) - thr) for j in range(w.P) if j != qb)
+                    r["margin"] = min(r.get("margin", float("inf")), m)
                 d = out.float() - fresh[qb]
                 drift.append(float(d.norm() / fresh[qb].norm()))
                 maxabs.append(float(d.abs().max()))
@@ -387,6 +393,7 @@ def planner_result(w, thresholds):
         out[str(thr)] = {"threshold": thr, "selective_ms_per_step": r["t"] / w.steps,
                          "all_fresh_ms_per_step": t_full / w.steps, "speedup_vs_all_fresh": t_full / r["t"],
                          "computed_fraction": r["flops"] / flops_full,
+                         "anchor_weight_margin_min": r.get("margin"),
                          "tflops_selective": r["flops"] / (r["t"] * 1e-3) / 1e12, "per_step": r["per_step"]}
     return {"workload": w.name, "steps": w.steps, "query_blocks": len(blocks), "anchors": list(w.anchors),
             "by_threshold": out,

@@ -146,6 +146,8 @@ def contrib(lse_states: torch.Tensor, lse_out: torch.Tensor, w_part: torch.Tenso
     """Per-row and per-partition contribution weights (ditango_contrib)."""
     _dev(lse_states, lse_out, w_part, workspace, w_rows)
     P, B, H, q_len = lse_states.shape
+    if lse_states.dtype != torch.float32 or lse_out.dtype != torch.float32:
+        raise ValueError("lse_states and lse_out must be float32")
     if tuple(lse_out.shape) != (B, H, q_len):
         raise ValueError("lse_out must be [B, H, q_len]")
     if tuple(w_part.shape) != (P,) or w_part.dtype != torch.float32:
@@ -168,6 +170,8 @@ def contrib_noalloc(lse_states: torch.Tensor, lse_out: torch.Tensor, w_part: tor
     scratch instead of a workspace (nothing is allocated)."""
     _dev(lse_states, lse_out, w_part, w_rows)
     P, B, H, q_len = lse_states.shape
+    if lse_states.dtype != torch.float32 or lse_out.dtype != torch.float32:
+        raise ValueError("lse_states and lse_out must be float32")
     if tuple(lse_out.shape) != (B, H, q_len):
         raise ValueError("lse_out must be [B, H, q_len]")
     if tuple(w_part.shape) != (P,) or w_part.dtype != torch.float32:
