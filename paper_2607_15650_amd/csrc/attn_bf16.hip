@@ -710,6 +710,235 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
   }
 }
 
+// ---------------------------------------------------------------------------
+// D=128 with the hand-scheduled key loop (attn_d128_loop.inc, written by
+// gen_attn_d128_loop.py, whose docstring describes the schedule).  One wave
+// per SIMD, two 32-row query blocks per wave: 4 waves, 256 query rows per
+// workgroup, 64-key tiles in a 4-deep LDS ring (K at 0, V at 64 KiB).  Task
+// decode, split units and the epilogue are those of attn_bf16_kernel; the
+// loop keeps every value in fixed registers, which the asm statement's
+// operands pin.
+#include "attn_d128_loop.inc"
+
+struct AsmD128 {
+  static constexpr int D = 128, QB = 2, NW = 4, BN = 64;
+  static constexpr int NT = NW * 64;
+  static constexpr int BM = NW * QB * 32;     // 256 rows, as the compiled kernel
+  static constexpr int ROWB = D * 2;
+  static constexpr int UNITS = D / 8;
+  static constexpr int ROWS_PER_LOAD = 1024 / ROWB;
+  static constexpr int RING = 131072;         // K ring (4 x 16 KiB), then V ring
+  static constexpr size_t LDS_BYTES = RING + 16;
+};
+
+// Buffer descriptor of raw bytes [base, base + nbytes): out-of-range loads
+// return zeros and do not access memory.  Word 3 selects 32-bit data format
+// for the gfx9 family.
+__device__ __forceinline__ u32x4 raw_buffer_desc(const void* base, uint32_t nbytes) {
+  const uint64_t p = (uint64_t)(uintptr_t)base;
+  return u32x4{(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p),
+               (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32)) & 0xffffu,
+               (uint32_t)__builtin_amdgcn_readfirstlane(nbytes), 0x00020000u};
+}
+
+template <typename TS>
+__global__ __launch_bounds__(256, 1) void attn_bf16_d128_asm_kernel(const AttnArgs a) {
+  using C = AsmD128;
+  constexpr int D = C::D, QB = C::QB, NW = C::NW, BN = C::BN;
+  extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+
+  int u;
+  if ((int)blockIdx.x < a.n_static) {
+    u = list_unit(a, (int)blockIdx.x & 7, (int)blockIdx.x >> 3);
+  } else {
+    int* claimed = (int*)(smem + C::RING);
+    if (threadIdx.x < 64) {
+      const int c = claim_unit(a, (int)threadIdx.x);
+      if (threadIdx.x == 0) *claimed = c;
+    }
+    __syncthreads();
+    u = __builtin_amdgcn_readfirstlane(*claimed);
+    if (u < 0) return;
+  }
+  int task = u, part = -1;
+  if (u >= a.n_main) {
+    task = a.n_main + (u - a.n_main) / a.split_f;
+    part = (u - a.n_main) % a.split_f;
+  }
+  const int qt = task % a.q_tiles;
+  int t = task / a.q_tiles;
+  const int h = t % a.H;
+  t /= a.H;
+  const int b = t % a.B;
+  const int sel = t / a.B;
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane & 31;
+  const int g = lane >> 5;
+
+  const int64_t HD = (int64_t)a.H * D;
+  int kv_len = a.kv_len[sel];
+  int64_t kv0 = a.kv_begin[sel];
+  const int slot = a.slot[sel];
+  if (part >= 0) {
+    const int per = ((kv_len + BN - 1) / BN + a.split_f - 1) / a.split_f * BN;
+    const int k0 = min(part * per, kv_len);
+    const int k1 = min(k0 + per, kv_len);
+    kv0 += k0;
+    kv_len = k1 - k0;
+  }
+  const int64_t row0 = (int64_t)qt * C::BM + wave * (QB * 32);
+  const uint32_t row_bytes = (uint32_t)HD * 2;
+
+  f32x16 o[QB][4];
+  float m[QB], l[QB];
+  if (kv_len > 0) {
+    const uint32_t smem_lds = lds_addr(smem);
+    const __bf16* kp = (const __bf16*)a.k + ((int64_t)b * a.S + kv0) * HD + (int64_t)h * D;
+    const __bf16* vp = (const __bf16*)a.v + ((int64_t)b * a.S + kv0) * HD + (int64_t)h * D;
+    // bytes from the partition's first key (this head) to the end of its last
+    const uint32_t nrec = (uint32_t)(kv_len - 1) * row_bytes + C::ROWB;
+    u32x4 kd = raw_buffer_desc(kp, nrec);
+    u32x4 vd = raw_buffer_desc(vp, nrec);
+    // this lane's LDS addresses: K fragment of k-step s (row lr, unit
+    // (2s+g) ^ swizzle), V^T transpose reads of dim block db
+    uint32_t kaddr[8], vaddr[4], dmak[4], dmav[4];
+#pragma unroll
+    for (int s = 0; s < 8; ++s) kaddr[s] = smem_lds + lr * C::ROWB + (uint32_t)(((2 * s + g) ^ swz_k<D>(lr)) * 16);
+    const int grp = lane >> 4, rr = lane & 15;
+    const int vrow = 4 * g + (rr >> 2);
+    const int vdim = 16 * (grp & 1) + 4 * (rr & 3);
+#pragma unroll
+    for (int db = 0; db < 4; ++db) {
+      const int dim = 32 * db + vdim;
+      vaddr[db] = smem_lds + C::RING / 2 + vrow * C::ROWB + (uint32_t)((((dim >> 3) ^ swz_v<D>(vrow))) * 16) + (dim & 7) * 2;
+    }
+    // tile loads: lane l of load j writes LDS unit l of the wave's j-th KiB
+    // (row l / 16 of the 4 the KiB holds, stored unit l % 16) from the
+    // global unit the swizzle maps there
+    const int ld_row = lane / C::UNITS, ld_unit = lane % C::UNITS;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = (wave * 4 + j) * C::ROWS_PER_LOAD + ld_row;
+      dmak[j] = row * row_bytes + (uint32_t)((ld_unit ^ swz_k<D>(row)) * 16);
+      dmav[j] = row * row_bytes + (uint32_t)((ld_unit ^ swz_v<D>(row)) * 16);
+    }
+    // the lane's Q rows (rows past q_len clamped: computed, never stored),
+    // advanced to dims 8g..8g+7
+    uint64_t qptr0, qptr1;
+    {
+      const __bf16* qb0 = (const __bf16*)a.q + ((int64_t)b * a.q_len + min(row0 + lr, a.q_len - 1)) * HD + (int64_t)h * D + 8 * g;
+      const __bf16* qb1 = (const __bf16*)a.q + ((int64_t)b * a.q_len + min(row0 + 32 + lr, a.q_len - 1)) * HD + (int64_t)h * D + 8 * g;
+      qptr0 = (uint64_t)(uintptr_t)qb0;
+      qptr1 = (uint64_t)(uintptr_t)qb1;
+    }
+    const float sl2 = a.scale_log2;
+    const uint32_t ntiles = (uint32_t)((kv_len + BN - 1) / BN);
+    const uint32_t kvl = (uint32_t)kv_len;
+    const uint32_t wv = (uint32_t)wave;
+    const uint32_t wlds = __builtin_amdgcn_readfirstlane(smem_lds + (uint32_t)wave * 4096u);
+    const uint32_t tileb = __builtin_amdgcn_readfirstlane(row_bytes * BN);
+    asm volatile(DITANGO_D128_LOOP_ASM
+                 : "={a[0:15]}"(o[0][0]), "={a[16:31]}"(o[0][1]), "={a[32:47]}"(o[0][2]), "={a[48:63]}"(o[0][3]),
+                   "={a[64:79]}"(o[1][0]), "={a[80:95]}"(o[1][1]), "={a[96:111]}"(o[1][2]), "={a[112:127]}"(o[1][3]),
+                   "={v230}"(m[0]), "={v231}"(m[1]), "={v232}"(l[0]), "={v233}"(l[1]),
+                   "+{s[48:51]}"(kd), "+{s[52:55]}"(vd), "+{v[64:65]}"(qptr0), "+{v[66:67]}"(qptr1)
+                 : "{v234}"(kaddr[0]), "{v235}"(kaddr[1]), "{v236}"(kaddr[2]), "{v237}"(kaddr[3]),
+                   "{v238}"(kaddr[4]), "{v239}"(kaddr[5]), "{v240}"(kaddr[6]), "{v241}"(kaddr[7]),
+                   "{v242}"(vaddr[0]), "{v243}"(vaddr[1]), "{v244}"(vaddr[2]), "{v245}"(vaddr[3]),
+                   "{v246}"(dmak[0]), "{v247}"(dmak[1]), "{v248}"(dmak[2]), "{v249}"(dmak[3]),
+                   "{v250}"(dmav[0]), "{v251}"(dmav[1]), "{v252}"(dmav[2]), "{v253}"(dmav[3]),
+                   "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s43}"(wv), "{s44}"(wlds), "{s45}"(tileb)
+                 : DITANGO_D128_LOOP_CLOBBERS);
+    // every wave's loads have landed and its reads of the ring are done
+    // before the ring is reused for the output rows
+    __syncthreads();
+  } else {
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      m[qb] = -INFINITY;
+      l[qb] = 0.f;
+#pragma unroll
+      for (int db = 0; db < 4; ++db) o[qb][db] = f32x16{};
+    }
+  }
+
+  // ---- epilogue (as attn_bf16_kernel): the wave's staging region is the
+  // start of its K ring slot
+  unsigned char* stage = smem + wave * (QB * 32 * C::ROWB);
+  auto swz_out = [](int row) { return row & (C::UNITS - 1); };
+  TS* outg = (TS*)a.out_states;
+  const int64_t slot_elems = (int64_t)a.B * a.q_len * HD;
+  const int64_t pt = part >= 0 ? (int64_t)(task - a.n_main) * a.split_f + part : 0;
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const float lt = pair_sum(l[qb]);
+    const int64_t row = row0 + qb * 32 + lr;
+    if (row < a.q_len) {
+      const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+      const float lse = lt > 0.f ? (m[qb] + __builtin_amdgcn_logf(lt)) * kLn2 : -INFINITY;
+      if (part < 0) {
+        if constexpr (sizeof(TS) == 2) {
+          unsigned char* srow = stage + (qb * 32 + lr) * C::ROWB;
+#pragma unroll
+          for (int db = 0; db < 4; ++db)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+              f32x4 x;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
+              const int unit = (4 * db + r4) ^ swz_out(qb * 32 + lr);
+              const int half = g ^ ((lr >> 4) & 1);
+              *(bf16x4*)(srow + unit * 16 + 8 * half) = __builtin_convertvector(x, bf16x4);
+            }
+        } else {
+          TS* dst = outg + (int64_t)slot * slot_elems + ((int64_t)b * a.q_len + row) * HD + (int64_t)h * D + 4 * g;
+#pragma unroll
+          for (int db = 0; db < 4; ++db)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+              f32x4 x;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
+              store4(dst + db * 32 + 8 * r4, x);
+            }
+        }
+        if (g == 0) a.lse_states[(((int64_t)slot * a.B + b) * a.H + h) * a.q_len + row] = lse;
+      } else {
+        const int64_t rl = row - (int64_t)qt * C::BM;
+        float* dst = a.part_out + (pt * C::BM + rl) * D + 4 * g;
+#pragma unroll
+        for (int db = 0; db < 4; ++db)
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) {
+            f32x4 x;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] = o[qb][db][4 * r4 + e] * inv;
+            store4(dst + db * 32 + 8 * r4, x);
+          }
+        if (g == 0) a.part_lse[pt * C::BM + rl] = lse;
+      }
+    }
+  }
+  if constexpr (sizeof(TS) == 2) {
+    if (part < 0) {
+      const int ld_row = lane / C::UNITS, ld_unit = lane % C::UNITS;
+      TS* dst0 = outg + (int64_t)slot * slot_elems + (int64_t)b * a.q_len * HD + (int64_t)h * D + ld_unit * 8;
+#pragma unroll
+      for (int i = 0; i < QB * 32 / C::ROWS_PER_LOAD; ++i) {
+        const int row = i * C::ROWS_PER_LOAD + ld_row;
+        if (row0 + row < a.q_len) {
+          bf16x8 x = *(const bf16x8*)(stage + row * C::ROWB + ((ld_unit ^ swz_out(row)) * 16));
+          if ((row >> 4) & 1) x = __builtin_shufflevector(x, x, 4, 5, 6, 7, 0, 1, 2, 3);
+          *(bf16x8*)(dst0 + (row0 + row) * HD) = x;
+        }
+      }
+    }
+  }
+}
+
 // Composes the split_f partial states of every split task (Eq. composition
 // over its key ranges) into the task's rows of its slot.  One thread per 8
 // elements of a row.
@@ -793,59 +1022,76 @@ struct Plan {
   size_t bytes = 0;         // kQueueBytes + split_bytes (0: nothing launched)
 };
 
+// A kernel of the launch below: the compiled form (any tile configuration)
+// or the hand-scheduled D=128 form.  Each names its function, workgroup
+// size, query rows per workgroup and dynamic LDS.
 template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
-hipError_t set_lds(size_t lds) {
-  static const hipError_t attr = hipFuncSetAttribute(
-      (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>,
-      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+struct CompiledKernel {
+  using C = Cfg<D, QB, NW, BN, NBUF>;
+  static constexpr int Dim = D, NT = C::NT, BM = C::BM, KEYS = BN;
+  static constexpr size_t LDS = C::LDS_BYTES;
+  static const void* fn() { return (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>; }
+  static void launch(dim3 grid, hipStream_t s, const AttnArgs& a) {
+    hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>), grid, dim3(NT), LDS, s, a);
+  }
+};
+
+template <typename TS>
+struct AsmKernelD128 {
+  static constexpr int Dim = 128, NT = AsmD128::NT, BM = AsmD128::BM, KEYS = AsmD128::BN;
+  static constexpr size_t LDS = AsmD128::LDS_BYTES;
+  static const void* fn() { return (const void*)attn_bf16_d128_asm_kernel<TS>; }
+  static void launch(dim3 grid, hipStream_t s, const AttnArgs& a) {
+    hipLaunchKernelGGL((attn_bf16_d128_asm_kernel<TS>), grid, dim3(NT), LDS, s, a);
+  }
+};
+
+template <class K>
+hipError_t set_lds() {
+  static const hipError_t attr = hipFuncSetAttribute(K::fn(), hipFuncAttributeMaxDynamicSharedMemorySize, (int)K::LDS);
   return attr;
 }
 
-template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
+template <class K>
 hipError_t plan_cfg(const AttnArgs& a, Plan* p) {
-  using C = Cfg<D, QB, NW, BN, NBUF>;
-  const size_t lds = C::LDS_BYTES;
-  hipError_t e = set_lds<D, QB, NW, BN, NBUF, WPE, SEQ, TS>(lds);
+  hipError_t e = set_lds<K>();
   if (e != hipSuccess) return e;
   *p = Plan{};
-  const int64_t nblk = (a.q_len + C::BM - 1) / C::BM * a.H * a.B * a.n_sel;
+  const int64_t nblk = (a.q_len + K::BM - 1) / K::BM * a.H * a.B * a.n_sel;
   if (nblk <= 0) return hipSuccess;
   int dev = 0, cus = 0, occ = 0;
   e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e == hipSuccess)
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &occ, (const void*)attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>, C::NT, lds);
+  if (e == hipSuccess) e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, K::fn(), K::NT, K::LDS);
   if (e != hipSuccess) return e;
   p->slots = (int64_t)cus * (occ > 0 ? occ : 1);
   p->bytes = kQueueBytes;
   // the split tasks are the launch's last ones: tiles of the last selected partition
-  const int64_t tiles = ((int64_t)a.kv_len[a.n_sel - 1] + BN - 1) / BN;
+  const int64_t tiles = ((int64_t)a.kv_len[a.n_sel - 1] + K::KEYS - 1) / K::KEYS;
   const int f = plan_tail_split(nblk, p->slots, tiles);
   if (f <= 1) return hipSuccess;
   p->f = f;
   p->n_split = nblk % p->slots;
-  p->split_bytes = align256((size_t)p->n_split * f * C::BM * D * sizeof(float)) +
-                   align256((size_t)p->n_split * f * C::BM * sizeof(float));
+  p->split_bytes = align256((size_t)p->n_split * f * K::BM * K::Dim * sizeof(float)) +
+                   align256((size_t)p->n_split * f * K::BM * sizeof(float));
   p->bytes += p->split_bytes;
   return hipSuccess;
 }
 
-template <int D, int QB, int NW, int BN, int NBUF, int WPE, bool SEQ, typename TS>
+template <class K, typename TS>
 hipError_t launch_cfg(const AttnArgs& a0, void* ws, size_t ws_bytes, hipStream_t s) {
-  using C = Cfg<D, QB, NW, BN, NBUF>;
-  const size_t lds = C::LDS_BYTES;
+  constexpr int D = K::Dim;
   Plan p;
   const bool queued = ws != nullptr && ws_bytes >= kQueueBytes;
   if (queued) {
-    const hipError_t e = plan_cfg<D, QB, NW, BN, NBUF, WPE, SEQ, TS>(a0, &p);
+    const hipError_t e = plan_cfg<K>(a0, &p);
     if (e != hipSuccess) return e;
   } else {
-    const hipError_t e = set_lds<D, QB, NW, BN, NBUF, WPE, SEQ, TS>(lds);
+    const hipError_t e = set_lds<K>();
     if (e != hipSuccess) return e;
   }
   AttnArgs a = a0;
-  a.q_tiles = (int)((a.q_len + C::BM - 1) / C::BM);
+  a.q_tiles = (int)((a.q_len + K::BM - 1) / K::BM);
   const int64_t nblk = (int64_t)a.q_tiles * a.H * a.B * a.n_sel;
   if (nblk <= 0) return hipSuccess;
   if (nblk + (int64_t)kMaxSplit * p.n_split + p.slots > 0x7fffffff) return hipErrorInvalidConfiguration;
@@ -862,7 +1108,7 @@ hipError_t launch_cfg(const AttnArgs& a0, void* ws, size_t ws_bytes, hipStream_t
       a.n_split = (int)p.n_split;
       a.split_f = p.f;
       a.part_out = (float*)((char*)ws + kQueueBytes);
-      a.part_lse = (float*)((char*)a.part_out + align256((size_t)p.n_split * p.f * C::BM * D * sizeof(float)));
+      a.part_lse = (float*)((char*)a.part_out + align256((size_t)p.n_split * p.f * K::BM * D * sizeof(float)));
     }
     // static share: the first positions of every XCD queue, all but its
     // last DITANGO_DYN_ROUNDS rounds and at least the first round (which
@@ -889,14 +1135,23 @@ hipError_t launch_cfg(const AttnArgs& a0, void* ws, size_t ws_bytes, hipStream_t
       if (e != hipSuccess) return e;
     }
   }
-  hipLaunchKernelGGL((attn_bf16_kernel<D, QB, NW, BN, NBUF, WPE, SEQ, TS>), dim3((unsigned)grid), dim3(C::NT), lds,
-                     s, a);
+  K::launch(dim3((unsigned)grid), s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_split == 0) return e;
-  const int64_t chunks = (int64_t)a.n_split * C::BM * (D / 8);
-  hipLaunchKernelGGL((attn_split_fixup_kernel<D, C::BM, TS>), dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0,
+  const int64_t chunks = (int64_t)a.n_split * K::BM * (D / 8);
+  hipLaunchKernelGGL((attn_split_fixup_kernel<D, K::BM, TS>), dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0,
                      s, a);
   return hipGetLastError();
+}
+
+// The hand-scheduled D=128 loop bounds its tile loads with 32-bit buffer
+// descriptors: every selected partition's bytes for one head must stay
+// below 2^31.
+inline bool asm_d128_fits(const AttnArgs& a) {
+  const int64_t row_bytes = (int64_t)a.H * 128 * 2;
+  for (int j = 0; j < a.n_sel; ++j)
+    if ((int64_t)a.kv_len[j] * row_bytes >= ((int64_t)1 << 31)) return false;
+  return true;
 }
 
 }  // namespace
@@ -914,15 +1169,27 @@ hipError_t launch_cfg(const AttnArgs& a0, void* ws, size_t ws_bytes, hipStream_t
 #ifndef DITANGO_D64_CFG
 #define DITANGO_D64_CFG 1, 12, 96, 2, 3, true
 #endif
+// D=128 runs the hand-scheduled kernel (attn_bf16_d128_asm_kernel) unless
+// built with DITANGO_D128_ASM=0, or a partition is too long for its 32-bit
+// tile-load bounds.
+#ifndef DITANGO_D128_ASM
+#define DITANGO_D128_ASM 1
+#endif
 
 hipError_t launch_attn_bf16_ws(const AttnArgs& a, int D, bool state_f32, void* ws, size_t ws_bytes,
                                hipStream_t s) {
-  if (D == 128)
-    return state_f32 ? launch_cfg<128, DITANGO_D128_CFG, float>(a, ws, ws_bytes, s)
-                     : launch_cfg<128, DITANGO_D128_CFG, __bf16>(a, ws, ws_bytes, s);
+  if (D == 128) {
+#if DITANGO_D128_ASM
+    if (asm_d128_fits(a))
+      return state_f32 ? launch_cfg<AsmKernelD128<float>, float>(a, ws, ws_bytes, s)
+                       : launch_cfg<AsmKernelD128<__bf16>, __bf16>(a, ws, ws_bytes, s);
+#endif
+    return state_f32 ? launch_cfg<CompiledKernel<128, DITANGO_D128_CFG, float>, float>(a, ws, ws_bytes, s)
+                     : launch_cfg<CompiledKernel<128, DITANGO_D128_CFG, __bf16>, __bf16>(a, ws, ws_bytes, s);
+  }
   if (D == 64)
-    return state_f32 ? launch_cfg<64, DITANGO_D64_CFG, float>(a, ws, ws_bytes, s)
-                     : launch_cfg<64, DITANGO_D64_CFG, __bf16>(a, ws, ws_bytes, s);
+    return state_f32 ? launch_cfg<CompiledKernel<64, DITANGO_D64_CFG, float>, float>(a, ws, ws_bytes, s)
+                     : launch_cfg<CompiledKernel<64, DITANGO_D64_CFG, __bf16>, __bf16>(a, ws, ws_bytes, s);
   return hipErrorInvalidValue;
 }
 
@@ -936,8 +1203,15 @@ hipError_t attn_bf16_ws_bytes(const AttnArgs& a, int D, size_t* bytes) {
   // the plan depends on the kernel's occupancy, which the state type does
   // not change; the bf16-state instantiation is queried
   hipError_t e = hipErrorInvalidValue;
-  if (D == 128) e = plan_cfg<128, DITANGO_D128_CFG, __bf16>(a, &p);
-  if (D == 64) e = plan_cfg<64, DITANGO_D64_CFG, __bf16>(a, &p);
+  if (D == 128) {
+#if DITANGO_D128_ASM
+    if (asm_d128_fits(a))
+      e = plan_cfg<AsmKernelD128<__bf16>>(a, &p);
+    else
+#endif
+      e = plan_cfg<CompiledKernel<128, DITANGO_D128_CFG, __bf16>>(a, &p);
+  }
+  if (D == 64) e = plan_cfg<CompiledKernel<64, DITANGO_D64_CFG, __bf16>>(a, &p);
   if (e == hipSuccess) *bytes = p.bytes;
   return e;
 }
