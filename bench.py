@@ -39,11 +39,11 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # elementwise copy reads / writes 1 GiB), keyed by the build id (source and
 # compile options) of the kernel they were taken on; reported only while the
 # build id matches.
-ATTN_TRAFFIC = {"build_id": "31d9b98986c5dac1", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "queue",
+ATTN_TRAFFIC = {"build_id": "77c398ba77fb985d", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "queue",
                 # the balanced attention kernel (mean of 5 launches: the order
                 # in which tasks are claimed moves the reads by up to 1 %); the
                 # counter reset moves about 1 KiB
-                "fetch_bytes": 762545.16 * 1024 * 2.0, "write_bytes": 287971.86 * 1024 * 1.0}
+                "fetch_bytes": 767017.2 * 1024 * 2.0, "write_bytes": 287960.2 * 1024 * 1.0}
 
 
 def parse():
@@ -103,7 +103,7 @@ def algorithmic(w, select):
 # rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_LDS_BANK_CONFLICT
 # (busy fraction = busy cycles / (1024 SIMDs x GRBM cycles / 8 XCDs); clock =
 # GRBM cycles / 8 / the traced kernel duration); reported under the same rule.
-ATTN_COUNTERS = {"mfma_busy": 0.636, "lds_bank_conflicts": 2269440, "clock_ghz": 1.83}
+ATTN_COUNTERS = {"mfma_busy": 0.772, "lds_bank_conflicts": 2269440, "clock_ghz": 1.71}
 
 
 # HBM bytes per launch of the merge kernel at the default workload (all P
@@ -128,10 +128,13 @@ def attn_mode(ws):
     return "split" if ws.numel() > 256 else "queue"
 
 
-def attn_kernels(ws):
+def attn_kernels(ws, D=128):
+    """The kernels of one attention launch: D=128 runs the hand-scheduled
+    kernel (attn_bf16_d128_asm_kernel), D=64 the compiled one."""
     mode = attn_mode(ws)
-    return {"static": "attn_bf16_kernel", "queue": "attn_queue_reset_kernel + attn_bf16_kernel",
-            "split": "attn_queue_reset_kernel + attn_bf16_kernel + attn_split_fixup_kernel"}[mode]
+    k = "attn_bf16_d128_asm_kernel" if D == 128 else "attn_bf16_kernel"
+    return {"static": k, "queue": f"attn_queue_reset_kernel + {k}",
+            "split": f"attn_queue_reset_kernel + {k} + attn_split_fixup_kernel"}[mode]
 
 
 def attn_counters(w, select, mode):
@@ -796,7 +799,7 @@ def main():
                    "attn_launch": attn_mode(ws_attn), "step_graph": bool(args.graph),
                    "attn_workspace_bytes": int(ws_attn.numel()) if ws_attn is not None else 0},
         "roofline": {"bound": "mfma",
-                     "kernel": attn_kernels(ws_attn) if w.dtype == "bf16" else "attn_f32_kernel",
+                     "kernel": attn_kernels(ws_attn, w.D) if w.dtype == "bf16" else "attn_f32_kernel",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": attn_traffic(w, select, attn_mode(ws_attn)),
                      "counters": attn_counters(w, select, attn_mode(ws_attn))},

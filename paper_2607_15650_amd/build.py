@@ -44,12 +44,19 @@ def flags():
     return CODEGEN_FLAGS + ["-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-function"]
 
 
+# generated code a source includes besides internal.h
+INCLUDES = {"attn_bf16.hip": ["attn_d128_loop.inc"]}
+
+
 def source_id(name: str) -> str:
-    """SHA-256 prefix over a source file and the options it is compiled with:
-    changes whenever the code built from it can change."""
+    """SHA-256 prefix over a source file, the files it includes from csrc/
+    and the options it is compiled with: changes whenever the code built
+    from it can change."""
     import hashlib
     h = hashlib.sha256(open(os.path.join(CSRC, name), "rb").read())
     h.update(open(os.path.join(CSRC, "internal.h"), "rb").read())
+    for inc in INCLUDES.get(name, []):
+        h.update(open(os.path.join(CSRC, inc), "rb").read())
     h.update(" ".join(CODEGEN_FLAGS + SOURCE_FLAGS.get(name, [])).encode())
     return h.hexdigest()[:16]
 

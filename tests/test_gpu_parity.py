@@ -221,6 +221,9 @@ EDGE = [
     # exact multiples of the key tiles (64 at D=128, 96 at D=64) and of the
     # query tiles (256 rows at D=128, 384 at D=64), and one key either side
     ("bf16", 128, 2, 256, [64, 128, 63, 65]),
+    # 3, 3, 5, 6, 7 and 9 key tiles: the D=128 loop ends in each of its four
+    # unrolled positions and masks a partial last tile from each of them
+    ("bf16", 128, 2, 300, [130, 192, 300, 321, 440, 513]),
     ("bf16", 64, 4, 384, [96, 192, 95, 97]),
     ("bf16", 64, 1, 385, [288, 1, 383]),
     ("f32", 128, 2, 129, [31, 33, 96]),
