@@ -128,11 +128,16 @@ def attn_mode(ws):
     return "split" if ws.numel() > 256 else "queue"
 
 
-def attn_kernels(ws, D=128):
-    """The kernels of one attention launch: D=128 runs the hand-scheduled
-    kernel (attn_bf16_d128_asm_kernel), D=64 the compiled one."""
+def attn_kernels(ws, w, select):
+    """The kernels of one attention launch: the hand-scheduled kernel at
+    D=128, and at D=64 for launches of at least four rounds of 256-row tasks
+    (shorter D=64 launches run the compiled kernel)."""
+    import torch
     mode = attn_mode(ws)
-    k = "attn_bf16_d128_asm_kernel" if D == 128 else "attn_bf16_kernel"
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    tasks = -(-w.q_len // 256) * w.H * w.B * len(select)
+    asm = w.D == 128 or tasks >= 4 * cus
+    k = f"attn_bf16_asm_kernel<{w.D}>" if asm else f"attn_bf16_kernel<{w.D}>"
     return {"static": k, "queue": f"attn_queue_reset_kernel + {k}",
             "split": f"attn_queue_reset_kernel + {k} + attn_split_fixup_kernel"}[mode]
 
@@ -799,7 +804,7 @@ def main():
                    "attn_launch": attn_mode(ws_attn), "step_graph": bool(args.graph),
                    "attn_workspace_bytes": int(ws_attn.numel()) if ws_attn is not None else 0},
         "roofline": {"bound": "mfma",
-                     "kernel": attn_kernels(ws_attn, w.D) if w.dtype == "bf16" else "attn_f32_kernel",
+                     "kernel": attn_kernels(ws_attn, w, select) if w.dtype == "bf16" else "attn_f32_kernel",
                      "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": attn_traffic(w, select, attn_mode(ws_attn)),
                      "counters": attn_counters(w, select, attn_mode(ws_attn))},

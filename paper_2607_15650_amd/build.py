@@ -45,7 +45,7 @@ def flags():
 
 
 # generated code a source includes besides internal.h
-INCLUDES = {"attn_bf16.hip": ["attn_d128_loop.inc"]}
+INCLUDES = {"attn_bf16.hip": ["attn_d128_loop.inc", "attn_d64_loop.inc"]}
 
 
 def source_id(name: str) -> str:

@@ -711,24 +711,31 @@ __global__ __launch_bounds__(NW * 64, WPE) void attn_bf16_kernel(const AttnArgs 
 }
 
 // ---------------------------------------------------------------------------
-// D=128 with the hand-scheduled key loop (attn_d128_loop.inc, written by
-// gen_attn_d128_loop.py, whose docstring describes the schedule).  One wave
-// per SIMD, two 32-row query blocks per wave: 4 waves, 256 query rows per
-// workgroup, 64-key tiles in a 4-deep LDS ring (K at 0, V at 64 KiB).  Task
+// The hand-scheduled key loop (attn_d128_loop.inc, attn_d64_loop.inc, written
+// by gen_attn_loop.py, whose docstring describes the schedule).  One wave per
+// SIMD, two 32-row query blocks per wave: 4 waves, 256 query rows per
+// workgroup, 64-key tiles in a 4-deep LDS ring (K first, then V).  Task
 // decode, split units and the epilogue are those of attn_bf16_kernel; the
 // loop keeps every value in fixed registers, which the asm statement's
 // operands pin.
 #include "attn_d128_loop.inc"
+#include "attn_d64_loop.inc"
 
-struct AsmD128 {
-  static constexpr int D = 128, QB = 2, NW = 4, BN = 64;
+template <int D_>
+struct AsmCfg {
+  static constexpr int D = D_, QB = 2, NW = 4, BN = 64;
   static constexpr int NT = NW * 64;
-  static constexpr int BM = NW * QB * 32;     // 256 rows, as the compiled kernel
+  static constexpr int BM = NW * QB * 32;     // 256 rows
+  static constexpr int KS = D / 16;           // MFMA k-steps over the head dim
+  static constexpr int DB = D / 32;           // 32-dim blocks of the output
   static constexpr int ROWB = D * 2;
   static constexpr int UNITS = D / 8;
   static constexpr int ROWS_PER_LOAD = 1024 / ROWB;
-  static constexpr int RING = 131072;         // K ring (4 x 16 KiB), then V ring
+  static constexpr int TILEB = BN * ROWB;
+  static constexpr int LW = TILEB / 1024 / NW;   // 1 KiB loads per wave per tile
+  static constexpr int RING = 8 * TILEB;      // K ring (4 tiles), then V ring (4 tiles)
   static constexpr size_t LDS_BYTES = RING + 16;
+  static_assert(QB * 32 * ROWB * NW <= RING, "output staging inside the ring");
 };
 
 // Buffer descriptor of raw bytes [base, base + nbytes): out-of-range loads
@@ -741,10 +748,10 @@ __device__ __forceinline__ u32x4 raw_buffer_desc(const void* base, uint32_t nbyt
                (uint32_t)__builtin_amdgcn_readfirstlane(nbytes), 0x00020000u};
 }
 
-template <typename TS>
-__global__ __launch_bounds__(256, 1) void attn_bf16_d128_asm_kernel(const AttnArgs a) {
-  using C = AsmD128;
-  constexpr int D = C::D, QB = C::QB, NW = C::NW, BN = C::BN;
+template <int D_, typename TS>
+__global__ __launch_bounds__(256, 1) void attn_bf16_asm_kernel(const AttnArgs a) {
+  using C = AsmCfg<D_>;
+  constexpr int D = C::D, QB = C::QB, BN = C::BN, KS = C::KS, DB = C::DB, LW = C::LW;
   extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
 
   int u;
@@ -792,7 +799,7 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_d128_asm_kernel(const AttnAr
   const int64_t row0 = (int64_t)qt * C::BM + wave * (QB * 32);
   const uint32_t row_bytes = (uint32_t)HD * 2;
 
-  f32x16 o[QB][4];
+  f32x16 o[QB][DB];
   float m[QB], l[QB];
   if (kv_len > 0) {
     const uint32_t smem_lds = lds_addr(smem);
@@ -804,24 +811,24 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_d128_asm_kernel(const AttnAr
     u32x4 vd = raw_buffer_desc(vp, nrec);
     // this lane's LDS addresses: K fragment of k-step s (row lr, unit
     // (2s+g) ^ swizzle), V^T transpose reads of dim block db
-    uint32_t kaddr[8], vaddr[4], dmak[4], dmav[4];
+    uint32_t kaddr[KS], vaddr[DB], dmak[LW], dmav[LW];
 #pragma unroll
-    for (int s = 0; s < 8; ++s) kaddr[s] = smem_lds + lr * C::ROWB + (uint32_t)(((2 * s + g) ^ swz_k<D>(lr)) * 16);
+    for (int s = 0; s < KS; ++s) kaddr[s] = smem_lds + lr * C::ROWB + (uint32_t)(((2 * s + g) ^ swz_k<D>(lr)) * 16);
     const int grp = lane >> 4, rr = lane & 15;
     const int vrow = 4 * g + (rr >> 2);
     const int vdim = 16 * (grp & 1) + 4 * (rr & 3);
 #pragma unroll
-    for (int db = 0; db < 4; ++db) {
+    for (int db = 0; db < DB; ++db) {
       const int dim = 32 * db + vdim;
       vaddr[db] = smem_lds + C::RING / 2 + vrow * C::ROWB + (uint32_t)((((dim >> 3) ^ swz_v<D>(vrow))) * 16) + (dim & 7) * 2;
     }
     // tile loads: lane l of load j writes LDS unit l of the wave's j-th KiB
-    // (row l / 16 of the 4 the KiB holds, stored unit l % 16) from the
-    // global unit the swizzle maps there
+    // (row l / UNITS of the ROWS_PER_LOAD the KiB holds, stored unit
+    // l % UNITS) from the global unit the swizzle maps there
     const int ld_row = lane / C::UNITS, ld_unit = lane % C::UNITS;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = (wave * 4 + j) * C::ROWS_PER_LOAD + ld_row;
+    for (int j = 0; j < LW; ++j) {
+      const int row = (wave * LW + j) * C::ROWS_PER_LOAD + ld_row;
       dmak[j] = row * row_bytes + (uint32_t)((ld_unit ^ swz_k<D>(row)) * 16);
       dmav[j] = row * row_bytes + (uint32_t)((ld_unit ^ swz_v<D>(row)) * 16);
     }
@@ -838,20 +845,32 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_d128_asm_kernel(const AttnAr
     const uint32_t ntiles = (uint32_t)((kv_len + BN - 1) / BN);
     const uint32_t kvl = (uint32_t)kv_len;
     const uint32_t wv = (uint32_t)wave;
-    const uint32_t wlds = __builtin_amdgcn_readfirstlane(smem_lds + (uint32_t)wave * 4096u);
+    const uint32_t wlds = __builtin_amdgcn_readfirstlane(smem_lds + (uint32_t)wave * (LW * 1024u));
     const uint32_t tileb = __builtin_amdgcn_readfirstlane(row_bytes * BN);
-    asm volatile(DITANGO_D128_LOOP_ASM
-                 : "={a[0:15]}"(o[0][0]), "={a[16:31]}"(o[0][1]), "={a[32:47]}"(o[0][2]), "={a[48:63]}"(o[0][3]),
-                   "={a[64:79]}"(o[1][0]), "={a[80:95]}"(o[1][1]), "={a[96:111]}"(o[1][2]), "={a[112:127]}"(o[1][3]),
-                   "={v230}"(m[0]), "={v231}"(m[1]), "={v232}"(l[0]), "={v233}"(l[1]),
-                   "+{s[48:51]}"(kd), "+{s[52:55]}"(vd), "+{v[64:65]}"(qptr0), "+{v[66:67]}"(qptr1)
-                 : "{v234}"(kaddr[0]), "{v235}"(kaddr[1]), "{v236}"(kaddr[2]), "{v237}"(kaddr[3]),
-                   "{v238}"(kaddr[4]), "{v239}"(kaddr[5]), "{v240}"(kaddr[6]), "{v241}"(kaddr[7]),
-                   "{v242}"(vaddr[0]), "{v243}"(vaddr[1]), "{v244}"(vaddr[2]), "{v245}"(vaddr[3]),
-                   "{v246}"(dmak[0]), "{v247}"(dmak[1]), "{v248}"(dmak[2]), "{v249}"(dmak[3]),
-                   "{v250}"(dmav[0]), "{v251}"(dmav[1]), "{v252}"(dmav[2]), "{v253}"(dmav[3]),
-                   "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s43}"(wv), "{s44}"(wlds), "{s45}"(tileb)
-                 : DITANGO_D128_LOOP_CLOBBERS);
+    if constexpr (D == 128) {
+      asm volatile(DITANGO_D128_LOOP_ASM
+                   : "={a[0:15]}"(o[0][0]), "={a[16:31]}"(o[0][1]), "={a[32:47]}"(o[0][2]), "={a[48:63]}"(o[0][3]),
+                     "={a[64:79]}"(o[1][0]), "={a[80:95]}"(o[1][1]), "={a[96:111]}"(o[1][2]), "={a[112:127]}"(o[1][3]),
+                     "={v230}"(m[0]), "={v231}"(m[1]), "={v232}"(l[0]), "={v233}"(l[1]),
+                     "+{s[48:51]}"(kd), "+{s[52:55]}"(vd), "+{v[64:65]}"(qptr0), "+{v[66:67]}"(qptr1)
+                   : "{v234}"(kaddr[0]), "{v235}"(kaddr[1]), "{v236}"(kaddr[2]), "{v237}"(kaddr[3]),
+                     "{v238}"(kaddr[4]), "{v239}"(kaddr[5]), "{v240}"(kaddr[6]), "{v241}"(kaddr[7]),
+                     "{v242}"(vaddr[0]), "{v243}"(vaddr[1]), "{v244}"(vaddr[2]), "{v245}"(vaddr[3]),
+                     "{v246}"(dmak[0]), "{v247}"(dmak[1]), "{v248}"(dmak[2]), "{v249}"(dmak[3]),
+                     "{v250}"(dmav[0]), "{v251}"(dmav[1]), "{v252}"(dmav[2]), "{v253}"(dmav[3]),
+                     "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s43}"(wv), "{s44}"(wlds), "{s45}"(tileb)
+                   : DITANGO_D128_LOOP_CLOBBERS);
+    } else {
+      asm volatile(DITANGO_D64_LOOP_ASM
+                   : "={a[0:15]}"(o[0][0]), "={a[16:31]}"(o[0][1]), "={a[32:47]}"(o[1][0]), "={a[48:63]}"(o[1][1]),
+                     "={v230}"(m[0]), "={v231}"(m[1]), "={v232}"(l[0]), "={v233}"(l[1]),
+                     "+{s[48:51]}"(kd), "+{s[52:55]}"(vd), "+{v[64:65]}"(qptr0), "+{v[66:67]}"(qptr1)
+                   : "{v234}"(kaddr[0]), "{v235}"(kaddr[1]), "{v236}"(kaddr[2]), "{v237}"(kaddr[3]),
+                     "{v238}"(vaddr[0]), "{v239}"(vaddr[1]), "{v240}"(dmak[0]), "{v241}"(dmak[1]),
+                     "{v242}"(dmav[0]), "{v243}"(dmav[1]),
+                     "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s43}"(wv), "{s44}"(wlds), "{s45}"(tileb)
+                   : DITANGO_D64_LOOP_CLOBBERS);
+    }
     // every wave's loads have landed and its reads of the ring are done
     // before the ring is reused for the output rows
     __syncthreads();
@@ -861,7 +880,7 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_d128_asm_kernel(const AttnAr
       m[qb] = -INFINITY;
       l[qb] = 0.f;
 #pragma unroll
-      for (int db = 0; db < 4; ++db) o[qb][db] = f32x16{};
+      for (int db = 0; db < DB; ++db) o[qb][db] = f32x16{};
     }
   }
 
@@ -883,7 +902,7 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_d128_asm_kernel(const AttnAr
         if constexpr (sizeof(TS) == 2) {
           unsigned char* srow = stage + (qb * 32 + lr) * C::ROWB;
 #pragma unroll
-          for (int db = 0; db < 4; ++db)
+          for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int r4 = 0; r4 < 4; ++r4) {
               f32x4 x;
@@ -896,7 +915,7 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_d128_asm_kernel(const AttnAr
         } else {
           TS* dst = outg + (int64_t)slot * slot_elems + ((int64_t)b * a.q_len + row) * HD + (int64_t)h * D + 4 * g;
 #pragma unroll
-          for (int db = 0; db < 4; ++db)
+          for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int r4 = 0; r4 < 4; ++r4) {
               f32x4 x;
@@ -910,7 +929,7 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_d128_asm_kernel(const AttnAr
         const int64_t rl = row - (int64_t)qt * C::BM;
         float* dst = a.part_out + (pt * C::BM + rl) * D + 4 * g;
 #pragma unroll
-        for (int db = 0; db < 4; ++db)
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
           for (int r4 = 0; r4 < 4; ++r4) {
             f32x4 x;
@@ -1036,13 +1055,14 @@ struct CompiledKernel {
   }
 };
 
-template <typename TS>
-struct AsmKernelD128 {
-  static constexpr int Dim = 128, NT = AsmD128::NT, BM = AsmD128::BM, KEYS = AsmD128::BN;
-  static constexpr size_t LDS = AsmD128::LDS_BYTES;
-  static const void* fn() { return (const void*)attn_bf16_d128_asm_kernel<TS>; }
+template <int D, typename TS>
+struct AsmKernel {
+  using C = AsmCfg<D>;
+  static constexpr int Dim = D, NT = C::NT, BM = C::BM, KEYS = C::BN;
+  static constexpr size_t LDS = C::LDS_BYTES;
+  static const void* fn() { return (const void*)attn_bf16_asm_kernel<D, TS>; }
   static void launch(dim3 grid, hipStream_t s, const AttnArgs& a) {
-    hipLaunchKernelGGL((attn_bf16_d128_asm_kernel<TS>), grid, dim3(NT), LDS, s, a);
+    hipLaunchKernelGGL((attn_bf16_asm_kernel<D, TS>), grid, dim3(NT), LDS, s, a);
   }
 };
 
@@ -1144,14 +1164,31 @@ hipError_t launch_cfg(const AttnArgs& a0, void* ws, size_t ws_bytes, hipStream_t
   return hipGetLastError();
 }
 
-// The hand-scheduled D=128 loop bounds its tile loads with 32-bit buffer
+// The hand-scheduled loops bound their tile loads with 32-bit buffer
 // descriptors: every selected partition's bytes for one head must stay
 // below 2^31.
-inline bool asm_d128_fits(const AttnArgs& a) {
-  const int64_t row_bytes = (int64_t)a.H * 128 * 2;
+inline bool asm_fits(const AttnArgs& a, int D) {
+  const int64_t row_bytes = (int64_t)a.H * D * 2;
   for (int j = 0; j < a.n_sel; ++j)
     if ((int64_t)a.kv_len[j] * row_bytes >= ((int64_t)1 << 31)) return false;
   return true;
+}
+
+// Which D=64 kernel a launch runs.  At D=64 the softmax's VALU work per MFMA
+// doubles and the hand-scheduled form gains little per tile (4 % at the
+// 118,800-token, 48-head shape), while its 256-row query tiles make more
+// tasks than the compiled kernel's 384-row ones: a launch that the compiled
+// kernel runs in one round can take two (the 16,384-token, 12-head reuse
+// launch: 288 tasks on 256 CUs against 216, 66.6 against 56 us).  So the
+// hand-scheduled kernel runs only launches of at least four rounds.
+inline bool d64_use_asm(const AttnArgs& a) {
+  if (!asm_fits(a, 64)) return false;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return false;
+  const int64_t tasks = (a.q_len + AsmCfg<64>::BM - 1) / AsmCfg<64>::BM * a.H * a.B * a.n_sel;
+  return tasks >= 4 * (int64_t)cus;
 }
 
 }  // namespace
@@ -1169,27 +1206,33 @@ inline bool asm_d128_fits(const AttnArgs& a) {
 #ifndef DITANGO_D64_CFG
 #define DITANGO_D64_CFG 1, 12, 96, 2, 3, true
 #endif
-// D=128 runs the hand-scheduled kernel (attn_bf16_d128_asm_kernel) unless
-// built with DITANGO_D128_ASM=0, or a partition is too long for its 32-bit
-// tile-load bounds.
-#ifndef DITANGO_D128_ASM
-#define DITANGO_D128_ASM 1
+// Both head dims run the hand-scheduled kernel (attn_bf16_asm_kernel) unless
+// built with DITANGO_ASM=0, or a partition is too long for its 32-bit
+// tile-load bounds, or (D=64) the launch is short (d64_use_asm).
+#ifndef DITANGO_ASM
+#define DITANGO_ASM 1
 #endif
 
 hipError_t launch_attn_bf16_ws(const AttnArgs& a, int D, bool state_f32, void* ws, size_t ws_bytes,
                                hipStream_t s) {
   if (D == 128) {
-#if DITANGO_D128_ASM
-    if (asm_d128_fits(a))
-      return state_f32 ? launch_cfg<AsmKernelD128<float>, float>(a, ws, ws_bytes, s)
-                       : launch_cfg<AsmKernelD128<__bf16>, __bf16>(a, ws, ws_bytes, s);
+#if DITANGO_ASM
+    if (asm_fits(a, 128))
+      return state_f32 ? launch_cfg<AsmKernel<128, float>, float>(a, ws, ws_bytes, s)
+                       : launch_cfg<AsmKernel<128, __bf16>, __bf16>(a, ws, ws_bytes, s);
 #endif
     return state_f32 ? launch_cfg<CompiledKernel<128, DITANGO_D128_CFG, float>, float>(a, ws, ws_bytes, s)
                      : launch_cfg<CompiledKernel<128, DITANGO_D128_CFG, __bf16>, __bf16>(a, ws, ws_bytes, s);
   }
-  if (D == 64)
+  if (D == 64) {
+#if DITANGO_ASM
+    if (d64_use_asm(a))
+      return state_f32 ? launch_cfg<AsmKernel<64, float>, float>(a, ws, ws_bytes, s)
+                       : launch_cfg<AsmKernel<64, __bf16>, __bf16>(a, ws, ws_bytes, s);
+#endif
     return state_f32 ? launch_cfg<CompiledKernel<64, DITANGO_D64_CFG, float>, float>(a, ws, ws_bytes, s)
                      : launch_cfg<CompiledKernel<64, DITANGO_D64_CFG, __bf16>, __bf16>(a, ws, ws_bytes, s);
+  }
   return hipErrorInvalidValue;
 }
 
@@ -1203,15 +1246,17 @@ hipError_t attn_bf16_ws_bytes(const AttnArgs& a, int D, size_t* bytes) {
   // the plan depends on the kernel's occupancy, which the state type does
   // not change; the bf16-state instantiation is queried
   hipError_t e = hipErrorInvalidValue;
-  if (D == 128) {
-#if DITANGO_D128_ASM
-    if (asm_d128_fits(a))
-      e = plan_cfg<AsmKernelD128<__bf16>>(a, &p);
-    else
+#if DITANGO_ASM
+  if (D == 128 && asm_fits(a, 128))
+    e = plan_cfg<AsmKernel<128, __bf16>>(a, &p);
+  else if (D == 64 && d64_use_asm(a))
+    e = plan_cfg<AsmKernel<64, __bf16>>(a, &p);
+  else
 #endif
-      e = plan_cfg<CompiledKernel<128, DITANGO_D128_CFG, __bf16>>(a, &p);
-  }
-  if (D == 64) e = plan_cfg<CompiledKernel<64, DITANGO_D64_CFG, __bf16>>(a, &p);
+  if (D == 128)
+    e = plan_cfg<CompiledKernel<128, DITANGO_D128_CFG, __bf16>>(a, &p);
+  else if (D == 64)
+    e = plan_cfg<CompiledKernel<64, DITANGO_D64_CFG, __bf16>>(a, &p);
   if (e == hipSuccess) *bytes = p.bytes;
   return e;
 }

@@ -1,5 +1,6 @@
-"""Writes attn_d128_loop.inc: the key loop of the D=128 bf16 attention kernel
-as one block of gfx950 assembly, scheduled by hand.
+"""Writes attn_d128_loop.inc and attn_d64_loop.inc: the key loop of the bf16
+attention kernel at head dim 128 and 64 as one block of gfx950 assembly
+each, scheduled by hand.
 
 The loop computes, for one task (256 query rows of one head against the keys
 of one partition), the unnormalised attention state of Sec. 2.2.4
@@ -29,7 +30,7 @@ the hand schedule adds is register placement and instruction order:
     tail mask and the load bursts are out of line.
 
 Register and LDS layout, the lazy running maximum and the accumulator layout
-of the 32x32x16 MFMA follow attn_bf16.hip.  Run `python gen_attn_d128_loop.py`
+of the 32x32x16 MFMA follow attn_bf16.hip.  Run `python gen_attn_loop.py`
 in this directory after editing; the build compiles the .inc as written.
 """
 from __future__ import annotations
@@ -75,22 +76,22 @@ def KADDR(s):                  # LDS byte address of this lane's K fragment, k-s
 
 
 def VADDR(db):                 # LDS byte address of this lane's V^T transpose reads, dim block db
-    return 242 + db
+    return 234 + KS + db
 
 
 def DMAK(j):                   # byte offset of this lane's 16 bytes in a K tile, load j
-    return 246 + j
+    return 234 + KS + DB + j
 
 
 def DMAV(j):
-    return 250 + j
+    return 234 + KS + DB + LW + j
 
 
 QPTR = 64                      # v[64:67]: the lane's Q row addresses, one per query block
 
 
 def O(qb, db):                 # AGPR accumulators of O^T
-    return 64 * qb + 16 * db
+    return 16 * DB * qb + 16 * db
 
 
 def Q(qb, s):                  # AGPR Q^T fragments
@@ -104,10 +105,29 @@ S_I, S_TMP, S_BIG, S_MASKAT, S_RET, S_CMP, S_NTM1 = 56, 57, 58, 59, 60, 62, 64
 SCRATCH_SGPRS = list(range(56, 65))
 
 KRING = 0                      # LDS byte offset of the K ring
-VRING = 65536                  # of the V ring (VADDR already includes it)
-TILEB = 16384                  # 64 keys x 256 bytes
-BURST_STEP = [0, 6, 12, 18]    # step before which wave w issues its loads
-BARRIER_STEP = 24
+
+
+def configure(d):
+    """Head dimension d (128 or 64): k-steps and dim blocks of the MFMAs, tile
+    bytes, 1 KiB loads per wave per tile, the V ring's offset, and where in
+    the iteration's steps the load bursts and the barrier sit."""
+    global D, KS, DB, ROWB, TILEB, LW, VRING, NQ, NP, BURST_STEP, BARRIER_STEP
+    D = d
+    KS, DB = d // 16, d // 32
+    ROWB = 2 * d                   # bytes per key row
+    TILEB = 64 * ROWB              # 64-key tile
+    LW = TILEB // 1024 // 4        # 1 KiB loads per wave per tile
+    VRING = 4 * TILEB              # the V ring follows the K ring (VADDR includes it)
+    NQ, NP = 2 * KS, 4 * DB        # score steps, P V steps
+    # the barrier that publishes the next tiles comes before the first read
+    # of the next iteration's K tile (issued LA steps before its step, right
+    # behind the first MFMA of a step, ahead of that step's events)
+    BARRIER_STEP = min(3 * (NQ + NP) // 4, NQ + NP - LA - 1)
+    BURST_STEP = [w * BARRIER_STEP // 4 for w in range(4)]
+    assert NQ + NP - LA > BARRIER_STEP and BURST_STEP[-1] < BARRIER_STEP
+
+
+configure(128)
 
 
 def kslot(t):
@@ -168,10 +188,10 @@ def qk_steps(nxt, t_next, buf0=0):
     """scores of tile t_next into S(nxt): 16 steps, k-step s outer, key block
     kb inner (an accumulator is reused every fourth MFMA)"""
     out = []
-    for s in range(8):
+    for s in range(KS):
         for kb in range(2):
             f = buf0 + 2 * s + kb
-            rd = [f"ds_read_b128 {v(FRAG(f), 4)}, {v(KADDR(s))} offset:{kslot(t_next) + kb * 8192}"]
+            rd = [f"ds_read_b128 {v(FRAG(f), 4)}, {v(KADDR(s))} offset:{kslot(t_next) + kb * 32 * ROWB}"]
             mf = []
             for qb in range(2):
                 src_c = "0" if s == 0 else v(S(nxt, kb, qb), 16)
@@ -180,19 +200,20 @@ def qk_steps(nxt, t_next, buf0=0):
     return out
 
 
-def pv_steps(cur, t_cur, buf0=16):
+def pv_steps(cur, t_cur, buf0=None):
     """O^T += V^T P^T over tile t_cur: 16 steps, key block kb, 16-key step s,
     dim block db (an accumulator is reused every eighth MFMA)"""
     out = []
     k = 0
+    buf0 = NQ if buf0 is None else buf0
     for kb in range(2):
         for s in (2 * kb, 2 * kb + 1):
-            for db in range(4):
+            for db in range(DB):
                 f = buf0 + k
                 k += 1
-                off = vslot(t_cur) + 16 * s * 256
+                off = vslot(t_cur) + 16 * s * ROWB
                 rd = [f"ds_read_b64_tr_b16 {v(FRAG(f), 2)}, {v(VADDR(db))} offset:{off}",
-                      f"ds_read_b64_tr_b16 {v(FRAG(f) + 2, 2)}, {v(VADDR(db))} offset:{off + 8 * 256}"]
+                      f"ds_read_b64_tr_b16 {v(FRAG(f) + 2, 2)}, {v(VADDR(db))} offset:{off + 8 * ROWB}"]
                 mf = [f"v_mfma_f32_32x32x16_bf16 {a_(O(qb, db), 16)}, {v(FRAG(f), 4)}, {v(P(cur, kb, qb, s % 2), 4)}, {a_(O(qb, db), 16)}"
                       for qb in range(2)]
                 out.append(Step(rd, mf))
@@ -267,7 +288,7 @@ def dma_tile(desc, ring_off, t):
     """this wave's four 1 KiB loads of a tile into ring slot t % 4"""
     out = []
     base = DMAK if desc == S_KD else DMAV
-    for j in range(4):
+    for j in range(LW):
         out.append(f"s_add_u32 m0, {s_(S_WLDS)}, {ring_off + (t % 4) * TILEB + j * 1024}")
         out.append("s_nop 0")
         out.append(f"buffer_load_dwordx4 {v(base(j))}, {s_(desc, 4)}, 0 offen lds")
@@ -346,22 +367,25 @@ def iteration(g, u):
     steps = qk_steps(nxt, u + 1) + pv_steps(cur, u)
     nxt_steps = qk_steps(cur, u + 2)[:LA]           # next iteration: S parity flips
     valu = {}
-    valu.update(spread_valu(sm_ops(cur, 1, 0, False), 0, 8))
-    valu.update(spread_valu(sm_ops(cur, 1, 1, False), 8, 8))
-    valu.update(spread_valu(sm_ops(nxt, 0, 0, True), 16, 8))
-    valu.update(spread_valu(sm_ops(nxt, 0, 1, True), 24, 8))
+    valu.update(spread_valu(sm_ops(cur, 1, 0, False), 0, NQ // 2))
+    valu.update(spread_valu(sm_ops(cur, 1, 1, False), NQ // 2, NQ // 2))
+    valu.update(spread_valu(sm_ops(nxt, 0, 0, True), NQ, NP // 2))
+    valu.update(spread_valu(sm_ops(nxt, 0, 1, True), NQ + NP // 2, NP // 2))
     events = {}
     for w in range(4):
         events.setdefault(BURST_STEP[w], []).extend(burst_event(g, w, u))
     # the test of tile i may redo its probabilities, and the mask changes
     # the scores of tile i+1: both before the first P V MFMA of tile i
-    pre = {16: check_event(g, cur) + mask_event(g, nxt)}
-    events.setdefault(BARRIER_STEP, []).extend(["s_waitcnt vmcnt(8)", "s_barrier"])
+    pre = {NQ: check_event(g, cur) + mask_event(g, nxt)}
+    # the wave's own loads of the previous tile pair have landed (only this
+    # iteration's burst, 2 LW loads, may be in flight)
+    events.setdefault(BARRIER_STEP, []).extend([f"s_waitcnt vmcnt({2 * LW})", "s_barrier"])
     # the iteration's scalar bookkeeping, spread over its last steps (after
     # every load burst), then the exit test
-    events.setdefault(28, []).extend(desc_advance(S_KD))
-    events.setdefault(29, []).extend(desc_advance(S_VD))
-    events.setdefault(30, []).extend([f"s_add_u32 {s_(S_I)}, {s_(S_I)}, 1"])
+    n = NQ + NP
+    events.setdefault(n - 4, []).extend(desc_advance(S_KD))
+    events.setdefault(n - 3, []).extend(desc_advance(S_VD))
+    events.setdefault(n - 2, []).extend([f"s_add_u32 {s_(S_I)}, {s_(S_I)}, 1"])
     g.lines += stream(steps, nxt_steps, valu, events, LA, pre)
     g.lines += [f"s_cmp_eq_u32 {s_(S_I)}, {s_(S_NTM1)}",
                 f"s_cbranch_scc1 {g.label(f'Llast{(u + 1) % 4}')}"]
@@ -375,7 +399,7 @@ def last_iteration(g, u):
     g.lines += [f"{g.label(f'Llast{u}')}:", "s_waitcnt lgkmcnt(0)"]
     g.lines += sm_ops(cur, 1, 0, False) + sm_ops(cur, 1, 1, False)
     g.lines += check_event(g, cur)
-    g.lines += ["s_waitcnt vmcnt(8)", "s_barrier"]
+    g.lines += [f"s_waitcnt vmcnt({2 * LW})", "s_barrier"]
     g.lines += stream(pv_steps(cur, u, 0), [], {}, {}, 0)
     g.lines += [f"s_branch {g.label('Ldone')}"]
 
@@ -407,7 +431,7 @@ def slow_block(g, par):
               f"v_cndmask_b32 {v(TMP + 2)}, {v(TMP + 2)}, 0, vcc",  # alpha (0 while m was -inf)
               f"v_mov_b32 {v(M(qb))}, {v(TMP)}",
               f"v_mul_f32 {v(L(qb))}, {v(L(qb))}, {v(TMP + 2)}"]
-        for k0 in range(0, 64, 16):
+        for k0 in range(0, 16 * DB, 16):
             for k in range(16):
                 c.append(f"v_accvgpr_read_b32 {v(X + k)}, {a_(O(qb, 0) + k0 + k)}")
             for k in range(16):
@@ -448,7 +472,7 @@ def prologue(g):
     L_ += ["s_nop 4"]
     for qb in range(2):
         L_ += [f"v_mov_b32 {v(M(qb))}, 0xff800000", f"v_mov_b32 {v(L(qb))}, 0"]
-    L_ += [f"v_accvgpr_write_b32 {a_(r)}, 0" for r in range(128)]
+    L_ += [f"v_accvgpr_write_b32 {a_(r)}, 0" for r in range(32 * DB)]
     L_ += [f"s_mov_b32 {s_(S_BIG)}, 0x53800000", f"s_mov_b32 {s_(S_I)}, 0",
            f"s_sub_u32 {s_(S_NTM1)}, {s_(S_NT)}, 1",
            # the steady iteration that masks the next tile: n-2 if the last tile is partial
@@ -461,11 +485,11 @@ def prologue(g):
         L_ += dma_tile(desc, ring, t) + desc_advance(desc)
     # Q^T fragments: 16 bytes per lane per (query block, k-step), into v0-v63
     for qb in range(2):
-        for s in range(8):
+        for s in range(KS):
             L_.append(f"global_load_dwordx4 {v(32 * qb + 4 * s, 4)}, {v(QPTR + 2 * qb, 2)}, off offset:{32 * s}")
     L_ += ["s_waitcnt vmcnt(0)"]
     for qb in range(2):
-        for s in range(8):
+        for s in range(KS):
             for j in range(4):
                 L_.append(f"v_accvgpr_write_b32 {a_(Q(qb, s) + j)}, {v(32 * qb + 4 * s + j)}")
     L_ += ["s_nop 2", "s_barrier"]
@@ -602,19 +626,20 @@ def check_fragments(lines):
     return problems
 
 
-def main():
+def write(d):
+    configure(d)
     lines = generate()
     probs = check_hazards(lines) + check_fragments(lines)
     if probs:
         print("\n".join(probs[:40]))
-        print(f"{len(probs)} problems")
+        print(f"D={d}: {len(probs)} problems")
         sys.exit(1)
     body = "\\n\\t".join(lines)
     here = os.path.dirname(os.path.abspath(__file__))
-    with open(os.path.join(here, "attn_d128_loop.inc"), "w") as f:
-        f.write("// Generated by gen_attn_d128_loop.py from the schedule described there.\n")
-        f.write(f"// {len(lines)} lines, {sum(1 for x in lines if x.startswith('v_mfma'))} MFMAs.\n")
-        f.write("#define DITANGO_D128_LOOP_ASM \\\n  \"")
+    with open(os.path.join(here, f"attn_d{d}_loop.inc"), "w") as f:
+        f.write("// Generated by gen_attn_loop.py from the schedule described there.\n")
+        f.write(f"// D={d}: {len(lines)} lines, {sum(1 for x in lines if x.startswith('v_mfma'))} MFMAs.\n")
+        f.write(f"#define DITANGO_D{d}_LOOP_ASM \\\n  \"")
         f.write(body)
         f.write("\\n\"\n")
         # registers the block writes besides its outputs: scores,
@@ -622,11 +647,16 @@ def main():
         # registers v64-v67 are in/out operands), the Q^T AGPRs, scalar
         # scratch
         clob = [f'"v{i}"' for i in range(0, 64)] + [f'"v{i}"' for i in range(68, 230)]
-        clob += [f'"a{i}"' for i in range(128, 192)]
+        clob += [f'"a{i}"' for i in range(128, Q(1, KS - 1) + 4)]
         clob += [f'"s{i}"' for i in SCRATCH_SGPRS]
         clob += ['"m0"', '"vcc"', '"scc"', '"memory"']
-        f.write("#define DITANGO_D128_LOOP_CLOBBERS \\\n  " + ", ".join(clob) + "\n")
-    print(f"{len(lines)} lines")
+        f.write(f"#define DITANGO_D{d}_LOOP_CLOBBERS \\\n  " + ", ".join(clob) + "\n")
+    print(f"D={d}: {len(lines)} lines")
+
+
+def main():
+    for d in (128, 64):
+        write(d)
 
 
 if __name__ == "__main__":

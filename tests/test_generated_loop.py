@@ -1,6 +1,6 @@
-"""The hand-scheduled D=128 key loop: the committed assembly is what its
-generator writes, and the generator's own checks hold and catch planted
-mistakes (CPU only)."""
+"""The hand-scheduled key loops (head dims 128 and 64): the committed
+assembly is what the generator writes, and the generator's own checks hold
+and catch planted mistakes (CPU only)."""
 import importlib.util
 import os
 
@@ -11,32 +11,39 @@ CSRC = os.path.join(os.path.dirname(HERE), "paper_2607_15650_amd", "csrc")
 
 
 def load_gen():
-    spec = importlib.util.spec_from_file_location("gen_attn_d128_loop", os.path.join(CSRC, "gen_attn_d128_loop.py"))
+    spec = importlib.util.spec_from_file_location("gen_attn_loop", os.path.join(CSRC, "gen_attn_loop.py"))
     m = importlib.util.module_from_spec(spec)
     spec.loader.exec_module(m)
     return m
 
 
-def committed_body():
-    text = open(os.path.join(CSRC, "attn_d128_loop.inc")).read()
-    start = text.index('#define DITANGO_D128_LOOP_ASM \\\n  "') + len('#define DITANGO_D128_LOOP_ASM \\\n  "')
+def committed_body(d):
+    text = open(os.path.join(CSRC, f"attn_d{d}_loop.inc")).read()
+    head = f'#define DITANGO_D{d}_LOOP_ASM \\\n  "'
+    start = text.index(head) + len(head)
     end = text.index('\\n"\n', start)
     return text[start:end].split("\\n\\t")
 
 
-def test_committed_loop_matches_generator():
+@pytest.mark.parametrize("d", [128, 64])
+def test_committed_loop_matches_generator(d):
     g = load_gen()
-    assert committed_body() == g.generate()
+    g.configure(d)
+    assert committed_body(d) == g.generate()
 
 
-def test_generated_loop_passes_its_checks():
+@pytest.mark.parametrize("d", [128, 64])
+def test_generated_loop_passes_its_checks(d):
     g = load_gen()
+    g.configure(d)
     lines = g.generate()
     assert g.check_hazards(lines) == []
     assert g.check_fragments(lines) == []
     mfma = [x for x in lines if x.startswith("v_mfma")]
-    # prologue 32, four unrolled iterations of 64, four last iterations of 32
-    assert len(mfma) == 32 + 4 * 64 + 4 * 32
+    # scores of tile 0, four unrolled iterations, four last iterations:
+    # 2 MFMAs per fragment step; D/8 score steps and D/8 P V steps per tile
+    steps = d // 8
+    assert len(mfma) == 2 * (steps + 4 * 2 * steps + 4 * steps)
     # every scalar register the block writes is declared scratch or is a pinned in/out operand
     written = set()
     for x in lines:

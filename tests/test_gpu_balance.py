@@ -13,7 +13,9 @@ from helpers import to_gpu
 
 pytestmark = pytest.mark.gpu
 
-ROWS = {128: 256, 64: 384}     # query rows per workgroup of each head dim's kernel
+# query rows per workgroup of the kernel each head dim's launches here run
+# (D=64 launches of fewer than four rounds run the compiled kernel)
+ROWS = {128: 256, 64: 384}
 
 
 def api():

@@ -218,13 +218,17 @@ EDGE = [
     ("bf16", 64, 2, 1, [7, 64, 129]),
     ("bf16", 128, 1, 257, [256, 255, 1]),
     ("bf16", 64, 5, 513, [100, 0, 333]),
-    # exact multiples of the key tiles (64 at D=128, 96 at D=64) and of the
-    # query tiles (256 rows at D=128, 384 at D=64), and one key either side
+    # exact multiples of the key tiles (64 keys) and of the
+    # query tiles (256 rows), and one key either side
     ("bf16", 128, 2, 256, [64, 128, 63, 65]),
-    # 3, 3, 5, 6, 7 and 9 key tiles: the D=128 loop ends in each of its four
+    # 3, 3, 5, 6, 7 and 9 key tiles: the loop ends in each of its four
     # unrolled positions and masks a partial last tile from each of them
     ("bf16", 128, 2, 300, [130, 192, 300, 321, 440, 513]),
-    ("bf16", 64, 4, 384, [96, 192, 95, 97]),
+    # the same at D=64, with enough heads for four rounds of tasks (the
+    # hand-scheduled D=64 kernel runs launches of at least four rounds)
+    ("bf16", 64, 128, 300, [130, 192, 300, 321, 440, 513]),
+    ("bf16", 64, 128, 257, [64, 128, 63, 65]),
+    ("bf16", 64, 4, 384, [96, 192, 95, 97]),    # 1.5 and 3 tiles of 64 keys, 1.5 query tiles
     ("bf16", 64, 1, 385, [288, 1, 383]),
     ("f32", 128, 2, 129, [31, 33, 96]),
     ("f32", 64, 3, 40, [0, 5, 70]),
