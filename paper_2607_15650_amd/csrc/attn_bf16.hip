@@ -738,6 +738,11 @@ struct AsmCfg {
   static_assert(QB * 32 * ROWB * NW <= RING, "output staging inside the ring");
 };
 
+// Bound on a lane's row sum below which the fast key loop's result is the
+// checked loop's, bit for bit (the checked loop raises m only for a tile
+// whose sum passes it).
+constexpr float kRowSumBound = 1099511627776.0f;   // 2^40
+
 // Buffer descriptor of raw bytes [base, base + nbytes): out-of-range loads
 // return zeros and do not access memory.  Word 3 selects 32-bit data format
 // for the gfx9 family.
@@ -803,12 +808,8 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_asm_kernel(const AttnArgs a)
   float m[QB], l[QB];
   if (kv_len > 0) {
     const uint32_t smem_lds = lds_addr(smem);
-    const __bf16* kp = (const __bf16*)a.k + ((int64_t)b * a.S + kv0) * HD + (int64_t)h * D;
-    const __bf16* vp = (const __bf16*)a.v + ((int64_t)b * a.S + kv0) * HD + (int64_t)h * D;
     // bytes from the partition's first key (this head) to the end of its last
     const uint32_t nrec = (uint32_t)(kv_len - 1) * row_bytes + C::ROWB;
-    u32x4 kd = raw_buffer_desc(kp, nrec);
-    u32x4 vd = raw_buffer_desc(vp, nrec);
     // this lane's LDS addresses: K fragment of k-step s (row lr, unit
     // (2s+g) ^ swizzle), V^T transpose reads of dim block db
     uint32_t kaddr[KS], vaddr[DB], dmak[LW], dmav[LW];
@@ -832,48 +833,84 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_asm_kernel(const AttnArgs a)
       dmak[j] = row * row_bytes + (uint32_t)((ld_unit ^ swz_k<D>(row)) * 16);
       dmav[j] = row * row_bytes + (uint32_t)((ld_unit ^ swz_v<D>(row)) * 16);
     }
-    // the lane's Q rows (rows past q_len clamped: computed, never stored),
-    // advanced to dims 8g..8g+7
-    uint64_t qptr0, qptr1;
-    {
-      const __bf16* qb0 = (const __bf16*)a.q + ((int64_t)b * a.q_len + min(row0 + lr, a.q_len - 1)) * HD + (int64_t)h * D + 8 * g;
-      const __bf16* qb1 = (const __bf16*)a.q + ((int64_t)b * a.q_len + min(row0 + 32 + lr, a.q_len - 1)) * HD + (int64_t)h * D + 8 * g;
-      qptr0 = (uint64_t)(uintptr_t)qb0;
-      qptr1 = (uint64_t)(uintptr_t)qb1;
-    }
     const float sl2 = a.scale_log2;
     const uint32_t ntiles = (uint32_t)((kv_len + BN - 1) / BN);
     const uint32_t kvl = (uint32_t)kv_len;
     const uint32_t wv = (uint32_t)wave;
     const uint32_t wlds = __builtin_amdgcn_readfirstlane(smem_lds + (uint32_t)wave * (LW * 1024u));
     const uint32_t tileb = __builtin_amdgcn_readfirstlane(row_bytes * BN);
-    if constexpr (D == 128) {
-      asm volatile(DITANGO_D128_LOOP_ASM
-                   : "={a[0:15]}"(o[0][0]), "={a[16:31]}"(o[0][1]), "={a[32:47]}"(o[0][2]), "={a[48:63]}"(o[0][3]),
-                     "={a[64:79]}"(o[1][0]), "={a[80:95]}"(o[1][1]), "={a[96:111]}"(o[1][2]), "={a[112:127]}"(o[1][3]),
-                     "={v230}"(m[0]), "={v231}"(m[1]), "={v232}"(l[0]), "={v233}"(l[1]),
-                     "+{s[48:51]}"(kd), "+{s[52:55]}"(vd), "+{v[64:65]}"(qptr0), "+{v[66:67]}"(qptr1)
-                   : "{v234}"(kaddr[0]), "{v235}"(kaddr[1]), "{v236}"(kaddr[2]), "{v237}"(kaddr[3]),
-                     "{v238}"(kaddr[4]), "{v239}"(kaddr[5]), "{v240}"(kaddr[6]), "{v241}"(kaddr[7]),
-                     "{v242}"(vaddr[0]), "{v243}"(vaddr[1]), "{v244}"(vaddr[2]), "{v245}"(vaddr[3]),
-                     "{v246}"(dmak[0]), "{v247}"(dmak[1]), "{v248}"(dmak[2]), "{v249}"(dmak[3]),
-                     "{v250}"(dmav[0]), "{v251}"(dmav[1]), "{v252}"(dmav[2]), "{v253}"(dmav[3]),
-                     "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s43}"(wv), "{s44}"(wlds), "{s45}"(tileb)
-                   : DITANGO_D128_LOOP_CLOBBERS);
-    } else {
-      asm volatile(DITANGO_D64_LOOP_ASM
-                   : "={a[0:15]}"(o[0][0]), "={a[16:31]}"(o[0][1]), "={a[32:47]}"(o[1][0]), "={a[48:63]}"(o[1][1]),
-                     "={v230}"(m[0]), "={v231}"(m[1]), "={v232}"(l[0]), "={v233}"(l[1]),
-                     "+{s[48:51]}"(kd), "+{s[52:55]}"(vd), "+{v[64:65]}"(qptr0), "+{v[66:67]}"(qptr1)
-                   : "{v234}"(kaddr[0]), "{v235}"(kaddr[1]), "{v236}"(kaddr[2]), "{v237}"(kaddr[3]),
-                     "{v238}"(vaddr[0]), "{v239}"(vaddr[1]), "{v240}"(dmak[0]), "{v241}"(dmak[1]),
-                     "{v242}"(dmav[0]), "{v243}"(dmav[1]),
-                     "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s43}"(wv), "{s44}"(wlds), "{s45}"(tileb)
-                   : DITANGO_D64_LOOP_CLOBBERS);
+    // Two forms of the key loop.  The fast one takes the running maximum m
+    // from tile 0 and keeps it; the checked one tests every tile and raises
+    // m (slow path) where a lane's tile sum passes 2^40 or is not a number.
+    // Both give m the same value at tile 0, so while no tile of the checked
+    // form would take the slow path the two agree bit for bit, and that is
+    // the case exactly when every lane's row sum (its tile sums added up)
+    // stays within 2^40: the fast form runs first, and a workgroup in which
+    // some lane's row sum left that range (or is NaN) runs its task again in
+    // the checked form.
+    int* redo = (int*)(smem + C::RING) + 1;
+    if (tid == 0) *redo = 0;
+    for (int pass = 0; pass < 2; ++pass) {
+      const __bf16* kp = (const __bf16*)a.k + ((int64_t)b * a.S + kv0) * HD + (int64_t)h * D;
+      const __bf16* vp = (const __bf16*)a.v + ((int64_t)b * a.S + kv0) * HD + (int64_t)h * D;
+      u32x4 kd = raw_buffer_desc(kp, nrec);
+      u32x4 vd = raw_buffer_desc(vp, nrec);
+      // the lane's Q rows (rows past q_len clamped: computed, never stored),
+      // advanced to dims 8g..8g+7
+      uint64_t qptr0, qptr1;
+      {
+        const __bf16* qb0 = (const __bf16*)a.q + ((int64_t)b * a.q_len + min(row0 + lr, a.q_len - 1)) * HD + (int64_t)h * D + 8 * g;
+        const __bf16* qb1 = (const __bf16*)a.q + ((int64_t)b * a.q_len + min(row0 + 32 + lr, a.q_len - 1)) * HD + (int64_t)h * D + 8 * g;
+        qptr0 = (uint64_t)(uintptr_t)qb0;
+        qptr1 = (uint64_t)(uintptr_t)qb1;
+      }
+      if constexpr (D == 128) {
+#define DITANGO_D128_CALL(BODY)                                                                                       \
+  asm volatile(BODY                                                                                                   \
+               : "={a[0:15]}"(o[0][0]), "={a[16:31]}"(o[0][1]), "={a[32:47]}"(o[0][2]), "={a[48:63]}"(o[0][3]),      \
+                 "={a[64:79]}"(o[1][0]), "={a[80:95]}"(o[1][1]), "={a[96:111]}"(o[1][2]), "={a[112:127]}"(o[1][3]),   \
+                 "={v230}"(m[0]), "={v231}"(m[1]), "={v232}"(l[0]), "={v233}"(l[1]),                                  \
+                 "+{s[48:51]}"(kd), "+{s[52:55]}"(vd), "+{v[64:65]}"(qptr0), "+{v[66:67]}"(qptr1)                     \
+               : "{v234}"(kaddr[0]), "{v235}"(kaddr[1]), "{v236}"(kaddr[2]), "{v237}"(kaddr[3]),                      \
+                 "{v238}"(kaddr[4]), "{v239}"(kaddr[5]), "{v240}"(kaddr[6]), "{v241}"(kaddr[7]),                      \
+                 "{v242}"(vaddr[0]), "{v243}"(vaddr[1]), "{v244}"(vaddr[2]), "{v245}"(vaddr[3]),                      \
+                 "{v246}"(dmak[0]), "{v247}"(dmak[1]), "{v248}"(dmak[2]), "{v249}"(dmak[3]),                          \
+                 "{v250}"(dmav[0]), "{v251}"(dmav[1]), "{v252}"(dmav[2]), "{v253}"(dmav[3]),                          \
+                 "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s43}"(wv), "{s44}"(wlds), "{s45}"(tileb)             \
+               : DITANGO_D128_LOOP_CLOBBERS)
+        if (pass == 0) {
+          DITANGO_D128_CALL(DITANGO_D128_FAST_ASM);
+        } else {
+          DITANGO_D128_CALL(DITANGO_D128_LOOP_ASM);
+        }
+#undef DITANGO_D128_CALL
+      } else {
+#define DITANGO_D64_CALL(BODY)                                                                                        \
+  asm volatile(BODY                                                                                                   \
+               : "={a[0:15]}"(o[0][0]), "={a[16:31]}"(o[0][1]), "={a[32:47]}"(o[1][0]), "={a[48:63]}"(o[1][1]),      \
+                 "={v230}"(m[0]), "={v231}"(m[1]), "={v232}"(l[0]), "={v233}"(l[1]),                                  \
+                 "+{s[48:51]}"(kd), "+{s[52:55]}"(vd), "+{v[64:65]}"(qptr0), "+{v[66:67]}"(qptr1)                     \
+               : "{v234}"(kaddr[0]), "{v235}"(kaddr[1]), "{v236}"(kaddr[2]), "{v237}"(kaddr[3]),                      \
+                 "{v238}"(vaddr[0]), "{v239}"(vaddr[1]), "{v240}"(dmak[0]), "{v241}"(dmak[1]),                        \
+                 "{v242}"(dmav[0]), "{v243}"(dmav[1]),                                                                \
+                 "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s43}"(wv), "{s44}"(wlds), "{s45}"(tileb)             \
+               : DITANGO_D64_LOOP_CLOBBERS)
+        if (pass == 0) {
+          DITANGO_D64_CALL(DITANGO_D64_FAST_ASM);
+        } else {
+          DITANGO_D64_CALL(DITANGO_D64_LOOP_ASM);
+        }
+#undef DITANGO_D64_CALL
+      }
+      // every wave's loads have landed and its reads of the ring are done
+      // before the ring is reused (output rows, or the checked pass)
+      __syncthreads();
+      if (pass == 1) break;
+      const bool over = !(l[0] <= kRowSumBound && l[1] <= kRowSumBound);
+      if (__builtin_amdgcn_ballot_w64(over) != 0 && lane == 0) *redo = 1;
+      __syncthreads();
+      if (__builtin_amdgcn_readfirstlane(*redo) == 0) break;
     }
-    // every wave's loads have landed and its reads of the ring are done
-    // before the ring is reused for the output rows
-    __syncthreads();
   } else {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {

@@ -305,7 +305,8 @@ def desc_advance(desc):
 
 # ---------------------------------------------------------------- generator
 class Gen:
-    def __init__(self):
+    def __init__(self, fast=False):
+        self.fast = fast          # the fast form: no per-tile test of the running maximum
         self.lines = []
         self.cold = []            # out-of-line code, emitted after the loop
         self.nlabel = 0
@@ -344,7 +345,12 @@ def burst_event(g, w, u):
 def check_event(g, par):
     """the lazy maximum test of tile i (parity par): a lane whose tile sum
     exceeds 2^40, or is not a number, sends the wave through the slow path;
-    then the tile sums join the row sums"""
+    then the tile sums join the row sums.  The fast form only adds the tile
+    sums: its maximum is tile 0's, and the kernel tests the row sums once,
+    after the loop (a row sum within 2^40 bounds every tile sum of the row)."""
+    if g.fast:
+        return [f"v_add_f32 {v(L(0))}, {v(L(0))}, {v(T(0))}",
+                f"v_add_f32 {v(L(1))}, {v(L(1))}, {v(T(1))}"]
     return ([f"v_cmp_nle_f32_e64 {s_(S_CMP, 2)}, {v(T(0))}, {s_(S_BIG)}",
              f"v_cmp_nle_f32_e64 vcc, {v(T(1))}, {s_(S_BIG)}",
              f"s_or_b64 vcc, vcc, {s_(S_CMP, 2)}"] +
@@ -467,6 +473,26 @@ def mask_block(g, par):
     c += ["s_nop 1", f"s_setpc_b64 {s_(S_RET, 2)}"]
 
 
+def tile0_max():
+    """m of each query block = scale*log2(e) times the row maximum of tile
+    0's scores (both key blocks, the two lanes of a row combined), the value
+    the slow path gives m at tile 0 in the checked form"""
+    out = []
+    for qb in range(2):
+        regs = [S(0, kb, qb) + r for kb in range(2) for r in range(16)]
+        out.append(f"v_max_f32 {v(TMP)}, {v(regs[0])}, {v(regs[1])}")
+        for r in regs[2:]:
+            out.append(f"v_max_f32 {v(TMP)}, {v(TMP)}, {v(r)}")
+        out += [f"v_mov_b32 {v(TMP + 1)}, {v(TMP)}",
+                "s_nop 1",
+                f"v_permlane32_swap_b32 {v(TMP)}, {v(TMP + 1)}",
+                "s_nop 1",
+                f"v_max_f32 {v(TMP)}, {v(TMP)}, {v(TMP + 1)}",
+                f"v_mul_f32 {v(TMP)}, {s_(S_SL2)}, {v(TMP)}",
+                f"v_max_f32 {v(M(qb))}, {v(M(qb))}, {v(TMP)}"]
+    return out + ["s_nop 2"]
+
+
 def prologue(g):
     L_ = g.lines
     L_ += ["s_nop 4"]
@@ -502,12 +528,14 @@ def prologue(g):
         f"s_cmp_eq_u32 {s_(S_TMP)}, 0",
         f"s_cbranch_scc1 {g.label('Lpmaskskip')}"] + g.call_seq(g.label("Lmask0")) + [f"{g.label('Lpmaskskip')}:"])
     L_ += ["s_nop 7", "s_nop 7"]
+    if g.fast:
+        L_ += tile0_max()
     L_ += sm_ops(0, 0, 0, True) + sm_ops(0, 0, 1, True)
     L_ += [f"s_cmp_eq_u32 {s_(S_NT)}, 1", f"s_cbranch_scc1 {g.label('Llast0')}"]
 
 
-def generate():
-    g = Gen()
+def generate(fast=False):
+    g = Gen(fast)
     prologue(g)
     g.lines += [f"{g.label('Lloop')}:"]
     for u in range(4):
@@ -516,7 +544,8 @@ def generate():
     for u in range(4):
         last_iteration(g, u)
     for par in range(2):
-        slow_block(g, par)
+        if not fast:
+            slow_block(g, par)
         mask_block(g, par)
     g.lines += g.cold
     g.lines += [f"{g.label('Ldone')}:", "s_waitcnt vmcnt(0) lgkmcnt(0)", "s_nop 7", "s_nop 7"]
@@ -628,20 +657,21 @@ def check_fragments(lines):
 
 def write(d):
     configure(d)
-    lines = generate()
-    probs = check_hazards(lines) + check_fragments(lines)
-    if probs:
-        print("\n".join(probs[:40]))
-        print(f"D={d}: {len(probs)} problems")
-        sys.exit(1)
-    body = "\\n\\t".join(lines)
+    forms = {"LOOP": generate(), "FAST": generate(fast=True)}
+    for name, lines in forms.items():
+        probs = check_hazards(lines) + check_fragments(lines)
+        if probs:
+            print("\n".join(probs[:40]))
+            print(f"D={d} {name}: {len(probs)} problems")
+            sys.exit(1)
     here = os.path.dirname(os.path.abspath(__file__))
     with open(os.path.join(here, f"attn_d{d}_loop.inc"), "w") as f:
         f.write("// Generated by gen_attn_loop.py from the schedule described there.\n")
-        f.write(f"// D={d}: {len(lines)} lines, {sum(1 for x in lines if x.startswith('v_mfma'))} MFMAs.\n")
-        f.write(f"#define DITANGO_D{d}_LOOP_ASM \\\n  \"")
-        f.write(body)
-        f.write("\\n\"\n")
+        for name, lines in forms.items():
+            f.write(f"// D={d} {name}: {len(lines)} lines, {sum(1 for x in lines if x.startswith('v_mfma'))} MFMAs.\n")
+            f.write(f"#define DITANGO_D{d}_{name}_ASM \\\n  \"")
+            f.write("\\n\\t".join(lines))
+            f.write("\\n\"\n")
         # registers the block writes besides its outputs: scores,
         # probabilities, fragments, temporaries, tile sums (the Q address
         # registers v64-v67 are in/out operands), the Q^T AGPRs, scalar
@@ -651,7 +681,7 @@ def write(d):
         clob += [f'"s{i}"' for i in SCRATCH_SGPRS]
         clob += ['"m0"', '"vcc"', '"scc"', '"memory"']
         f.write(f"#define DITANGO_D{d}_LOOP_CLOBBERS \\\n  " + ", ".join(clob) + "\n")
-    print(f"D={d}: {len(lines)} lines")
+    print(f"D={d}: {len(forms['LOOP'])} + {len(forms['FAST'])} lines")
 
 
 def main():

@@ -17,26 +17,55 @@ def load_gen():
     return m
 
 
-def committed_body(d):
+def committed_body(d, form="LOOP"):
     text = open(os.path.join(CSRC, f"attn_d{d}_loop.inc")).read()
-    head = f'#define DITANGO_D{d}_LOOP_ASM \\\n  "'
+    head = f'#define DITANGO_D{d}_{form}_ASM \\\n  "'
     start = text.index(head) + len(head)
     end = text.index('\\n"\n', start)
     return text[start:end].split("\\n\\t")
 
 
 @pytest.mark.parametrize("d", [128, 64])
-def test_committed_loop_matches_generator(d):
+@pytest.mark.parametrize("fast", [False, True])
+def test_committed_loop_matches_generator(d, fast):
     g = load_gen()
     g.configure(d)
-    assert committed_body(d) == g.generate()
+    assert committed_body(d, "FAST" if fast else "LOOP") == g.generate(fast=fast)
 
 
 @pytest.mark.parametrize("d", [128, 64])
-def test_generated_loop_passes_its_checks(d):
+def test_fast_form_differs_from_the_checked_one_only_in_the_maximum(d):
+    """The fast form has no per-tile test of the running maximum and no slow
+    path; its prologue sets m from tile 0's scores; every MFMA, LDS read,
+    tile load, wait and barrier is the checked form's, in the same order."""
     g = load_gen()
     g.configure(d)
-    lines = g.generate()
+    checked, fast = g.generate(), g.generate(fast=True)
+    assert not any(x.startswith("v_cmp_nle") for x in fast)
+    assert not any("Lslow" in x for x in fast)
+    assert sum(1 for x in checked if x.startswith("v_cmp_nle")) == 2 * 8   # 4 steady + 4 last iterations
+    keep = ("v_mfma", "ds_read", "buffer_load", "global_load", "s_waitcnt", "s_barrier")
+    pick = lambda lines: [x for x in lines if x.startswith(keep)]
+    assert pick(fast) == pick(checked)
+    # outside the prologue's maximum and the removed tests, the VALU work is
+    # the checked form's minus its slow blocks
+    exps = lambda lines: sum(1 for x in lines if x.startswith("v_exp"))
+    slow = checked[checked.index(".Lslow0_%=:"):]
+    assert exps(fast) == exps(checked) - exps(slow)
+    # tile 0's maximum: per query block, 31 maxima over its 32 scores, the
+    # lane pair's exchange, the scale, before the first exponential
+    first_exp = next(i for i, x in enumerate(fast) if x.startswith("v_exp"))
+    pro = fast[:first_exp]
+    assert sum(1 for x in pro if x.startswith("v_permlane32_swap")) == 2
+    assert sum(1 for x in pro if x.startswith("v_max_f32")) == 2 * (31 + 2)
+
+
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("fast", [False, True])
+def test_generated_loop_passes_its_checks(d, fast):
+    g = load_gen()
+    g.configure(d)
+    lines = g.generate(fast=fast)
     assert g.check_hazards(lines) == []
     assert g.check_fragments(lines) == []
     mfma = [x for x in lines if x.startswith("v_mfma")]

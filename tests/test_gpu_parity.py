@@ -411,6 +411,65 @@ def test_running_max_far_below_and_above(D):
 
 
 @pytest.mark.parametrize("D", [128, 64])
+def test_running_max_redo_in_a_long_launch(D):
+    """The hand-scheduled kernel runs a fast key loop that keeps tile 0's
+    maximum and, in a workgroup where a row sum left [0, 2^40], runs the task
+    again in the checked loop that raises the maximum.  A launch long enough
+    for the hand-scheduled kernel at both head dims (at least four rounds of
+    256-row tasks) with three heads whose later keys score far above tile 0
+    (queries scaled by 32; key norms rising, falling, jumping) and 61 plain
+    heads: tasks of both kinds in one launch, against the oracle on sampled
+    rows of every head, and bitwise equal on a second launch."""
+    import torch
+    a = api()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    rng = np.random.default_rng(7 + D)
+    B, H, dtype = 1, 64, "bf16"
+    lens = [700, 150]
+    S = sum(lens)
+    offs = [0, lens[0], S]
+    q_tiles = -(-4 * cus // (H * len(lens)))
+    q_len = q_tiles * 256 - 37
+    q = rng.standard_normal((B, q_len, H, D), dtype=np.float32)
+    q[:, :, :3, :] *= 32.0
+    k = rng.standard_normal((B, S, H, D), dtype=np.float32)
+    ramp = np.linspace(0.05, 1.0, S, dtype=np.float32)
+    k[:, :, 0, :] *= ramp[None, :, None]
+    k[:, :, 1, :] *= ramp[::-1][None, :, None]
+    k[:, :, 2, :] *= np.where(np.arange(S) < 400, 0.05, 1.0).astype(np.float32)[None, :, None]
+    v = rng.standard_normal((B, S, H, D), dtype=np.float32) * 0.25
+    scale = 1 / math.sqrt(D)
+    P = len(lens)
+    dq, dk, dv = to_gpu(q, dtype), to_gpu(k, dtype), to_gpu(v, dtype)
+    print(f"redo case D={D} H={H} q_len={q_len} tasks={q_tiles * H * P} cus={cus}", flush=True)
+    res = []
+    for _ in range(2):
+        out_states, lse_states = new_state_cache(P, B, q_len, H, D, dtype)
+        n_ws = a.attn_workspace_bytes(torch_dtype(dtype), B, H, D, q_len, offs, [1] * P)
+        ws = torch.empty(n_ws, dtype=torch.uint8, device="cuda") if n_ws > 0 else None
+        a.attn_partition_states(dq, dk, dv, offs, [1] * P, scale, out_states, lse_states, ws)
+        torch.cuda.synchronize()
+        res.append((out_states.float().cpu().numpy(), lse_states.cpu().numpy()))
+    assert np.array_equal(res[0][0], res[1][0]) and np.array_equal(res[0][1], res[1][1])
+    go, gl = res[0]
+    rows = np.unique(np.concatenate([[0, 1, 63, 64, 255, 256, q_len - 1],
+                                     rng.choice(q_len, 96, replace=False)]))
+    Q, K, V = (exact_inputs(t, dtype) for t in (q, k, v))
+    outs, lses = oracle.partition_states(Q[:, rows], K, V, offs, scale)
+    for j in range(P):
+        assert np.all(np.isfinite(go[j])) and np.all(np.isfinite(gl[j])), j
+        assert max_abs(go[j][:, rows], outs[j]) <= TOL[dtype]["out"], j
+        assert max_abs(gl[j][:, :, rows], lses[j]) <= TOL[dtype]["lse"], j
+    # premise: partition 0's top score lies far (> 128, base 2) above its first
+    # tile's in some row of the scaled heads, and within 30 in every row of
+    # the plain ones (their tasks keep the fast loop's result)
+    sc = np.einsum("bqhd,bkhd->bhqk", Q[:, rows], K[:, :lens[0]]) * scale
+    gap = (sc.max(axis=3) - sc[..., :64].max(axis=3)) / math.log(2.0)
+    assert gap[:, :3].max() > 128.0, gap[:, :3].max()
+    assert gap[:, 3:].max() < 30.0, gap[:, 3:].max()
+
+
+@pytest.mark.parametrize("D", [128, 64])
 def test_fp32_states_for_bf16_inputs(D):
     """bf16 inputs with the states kept in float32 (the _ex entry point): the
     states match the oracle, differ from the bf16 states by the bf16 store
