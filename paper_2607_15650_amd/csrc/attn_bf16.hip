@@ -825,13 +825,17 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_asm_kernel(const AttnArgs a)
     }
     // tile loads: lane l of load j writes LDS unit l of the wave's j-th KiB
     // (row l / UNITS of the ROWS_PER_LOAD the KiB holds, stored unit
-    // l % UNITS) from the global unit the swizzle maps there
+    // l % UNITS) from the global unit the swizzle maps there.  Load j carries
+    // j KiB as its immediate offset, which the hardware adds to the LDS
+    // destination and to the global address (and to the offset it range
+    // checks), so the lane's register holds its byte offset minus j KiB
+    // (never negative: the rows of the j-th KiB start j KiB of key rows in).
     const int ld_row = lane / C::UNITS, ld_unit = lane % C::UNITS;
 #pragma unroll
     for (int j = 0; j < LW; ++j) {
       const int row = (wave * LW + j) * C::ROWS_PER_LOAD + ld_row;
-      dmak[j] = row * row_bytes + (uint32_t)((ld_unit ^ swz_k<D>(row)) * 16);
-      dmav[j] = row * row_bytes + (uint32_t)((ld_unit ^ swz_v<D>(row)) * 16);
+      dmak[j] = row * row_bytes + (uint32_t)((ld_unit ^ swz_k<D>(row)) * 16) - 1024u * j;
+      dmav[j] = row * row_bytes + (uint32_t)((ld_unit ^ swz_v<D>(row)) * 16) - 1024u * j;
     }
     const float sl2 = a.scale_log2;
     const uint32_t ntiles = (uint32_t)((kv_len + BN - 1) / BN);

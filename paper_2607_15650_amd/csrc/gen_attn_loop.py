@@ -23,11 +23,16 @@ the hand schedule adds is register placement and instruction order:
     wait for a fragment where one group of MFMAs hands over to the next;
   * K and V tiles go into a 4-deep LDS ring with buffer loads that write LDS
     directly; the buffer descriptor ends at the partition's last key, so rows
-    past the end read as zeros without touching memory; each wave issues its
-    quarter of a tile pair at a different point of the iteration, so the
-    four waves' bursts do not coincide;
-  * the common path takes no branch: the slow path of the lazy maximum, the
-    tail mask and the load bursts are out of line.
+    past the end read as zeros without touching memory; every wave issues
+    its quarter of a tile pair one 1 KiB load at a time, spread over the
+    steps before the barrier, with one m0 per tile and the loads of a tile
+    at immediate offsets of 1 KiB (the offset moves both the global and the
+    LDS address, and the range check includes it);
+  * the steady loop takes no branch but its loop-back: iterations run in
+    blocks of four while none of the four is the last or masks a partial
+    last tile, and the tests for those two run only in the few iterations
+    after the blocks; the slow path of the lazy maximum and the tail mask
+    are out of line.
 
 Register and LDS layout, the lazy running maximum and the accumulator layout
 of the 32x32x16 MFMA follow attn_bf16.hip.  Run `python gen_attn_loop.py`
@@ -101,8 +106,8 @@ def Q(qb, s):                  # AGPR Q^T fragments
 # scalar registers: inputs pinned by the caller, then scratch
 S_SL2, S_NT, S_KVLEN, S_WAVE, S_WLDS, S_TILEB = 40, 41, 42, 43, 44, 45
 S_KD, S_VD = 48, 52            # buffer descriptors (4 each)
-S_I, S_TMP, S_BIG, S_MASKAT, S_RET, S_CMP, S_NTM1 = 56, 57, 58, 59, 60, 62, 64
-SCRATCH_SGPRS = list(range(56, 65))
+S_I, S_TMP, S_BIG, S_MASKAT, S_RET, S_CMP, S_NTM1, S_LIM = 56, 57, 58, 59, 60, 62, 64, 65
+SCRATCH_SGPRS = list(range(56, 66))
 
 KRING = 0                      # LDS byte offset of the K ring
 
@@ -110,8 +115,8 @@ KRING = 0                      # LDS byte offset of the K ring
 def configure(d):
     """Head dimension d (128 or 64): k-steps and dim blocks of the MFMAs, tile
     bytes, 1 KiB loads per wave per tile, the V ring's offset, and where in
-    the iteration's steps the load bursts and the barrier sit."""
-    global D, KS, DB, ROWB, TILEB, LW, VRING, NQ, NP, BURST_STEP, BARRIER_STEP
+    the iteration's steps the tile loads and the barrier sit."""
+    global D, KS, DB, ROWB, TILEB, LW, VRING, NQ, NP, LOAD_STEP, BARRIER_STEP
     D = d
     KS, DB = d // 16, d // 32
     ROWB = 2 * d                   # bytes per key row
@@ -123,8 +128,13 @@ def configure(d):
     # of the next iteration's K tile (issued LA steps before its step, right
     # behind the first MFMA of a step, ahead of that step's events)
     BARRIER_STEP = min(3 * (NQ + NP) // 4, NQ + NP - LA - 1)
-    BURST_STEP = [w * BARRIER_STEP // 4 for w in range(4)]
-    assert NQ + NP - LA > BARRIER_STEP and BURST_STEP[-1] < BARRIER_STEP
+    # the wave's 2 LW loads of an iteration (K, then V), one per step, spread
+    # over the steps before the barrier (measured: one load per event beats
+    # two or four, and branching to a per-wave burst cost about 8 % of the
+    # loop's cycles)
+    LOAD_STEP = [k * BARRIER_STEP // (2 * LW) for k in range(2 * LW)]
+    assert NQ + NP - LA > BARRIER_STEP and LOAD_STEP[-1] < BARRIER_STEP
+    assert len(set(LOAD_STEP)) == 2 * LW
 
 
 configure(128)
@@ -285,13 +295,18 @@ def spread_valu(ops, first_step, nsteps):
 
 # ---------------------------------------------------------------- loads
 def dma_tile(desc, ring_off, t):
-    """this wave's four 1 KiB loads of a tile into ring slot t % 4"""
-    out = []
+    """this wave's LW 1 KiB loads of a tile into ring slot t % 4, one list of
+    instructions per load: m0 is set to the wave's first KiB of the slot once,
+    and load j adds j KiB through its immediate offset, which moves the LDS
+    destination and the global address alike (the lane's offset register
+    holds its byte offset minus j KiB)"""
     base = DMAK if desc == S_KD else DMAV
+    out = [[f"s_add_u32 m0, {s_(S_WLDS)}, {ring_off + (t % 4) * TILEB}", "s_nop 0"]]
     for j in range(LW):
-        out.append(f"s_add_u32 m0, {s_(S_WLDS)}, {ring_off + (t % 4) * TILEB + j * 1024}")
-        out.append("s_nop 0")
-        out.append(f"buffer_load_dwordx4 {v(base(j))}, {s_(desc, 4)}, 0 offen lds")
+        off = f" offset:{1024 * j}" if j else ""
+        out[-1].append(f"buffer_load_dwordx4 {v(base(j))}, {s_(desc, 4)}, 0 offen{off} lds")
+        if j + 1 < LW:
+            out.append([])
     return out
 
 
@@ -336,10 +351,11 @@ class Gen:
         return [f"{cond_branch} {cold}", f"{back}:"]
 
 
-def burst_event(g, w, u):
-    """wave w's loads of iteration u (ring phase u % 4): K_{i+3} and V_{i+2}"""
-    body = dma_tile(S_KD, KRING, u + 3) + dma_tile(S_VD, VRING, u + 2)
-    return [f"s_cmp_eq_u32 {s_(S_WAVE)}, {w}"] + g.out_of_line("s_cbranch_scc1", body)
+def load_events(u):
+    """the wave's loads of iteration u (ring phase u % 4), K_{i+3} and
+    V_{i+2}, one per step of LOAD_STEP"""
+    loads = dma_tile(S_KD, KRING, u + 3) + dma_tile(S_VD, VRING, u + 2)
+    return {LOAD_STEP[k]: loads[k] for k in range(2 * LW)}
 
 
 def check_event(g, par):
@@ -366,9 +382,11 @@ def mask_event(g, nxt):
             g.out_of_line("s_cbranch_scc1", g.call_seq(g.label(f"Lmask{nxt}"))))
 
 
-def iteration(g, u):
+def iteration(g, u, tests=True):
     """steady iteration i (i % 4 == u): tile i+1 exists.  On entry the reads
-    of its first LA steps are issued; on exit those of the next iteration."""
+    of its first LA steps are issued; on exit those of the next iteration.
+    `tests`: the iteration may be the last steady one or the one that masks
+    a partial last tile (false inside the blocks of four)."""
     cur, nxt = u % 2, 1 - u % 2
     steps = qk_steps(nxt, u + 1) + pv_steps(cur, u)
     nxt_steps = qk_steps(cur, u + 2)[:LA]           # next iteration: S parity flips
@@ -378,23 +396,24 @@ def iteration(g, u):
     valu.update(spread_valu(sm_ops(nxt, 0, 0, True), NQ, NP // 2))
     valu.update(spread_valu(sm_ops(nxt, 0, 1, True), NQ + NP // 2, NP // 2))
     events = {}
-    for w in range(4):
-        events.setdefault(BURST_STEP[w], []).extend(burst_event(g, w, u))
+    for k, ins in load_events(u).items():
+        events.setdefault(k, []).extend(ins)
     # the test of tile i may redo its probabilities, and the mask changes
     # the scores of tile i+1: both before the first P V MFMA of tile i
-    pre = {NQ: check_event(g, cur) + mask_event(g, nxt)}
+    pre = {NQ: check_event(g, cur) + (mask_event(g, nxt) if tests else [])}
     # the wave's own loads of the previous tile pair have landed (only this
-    # iteration's burst, 2 LW loads, may be in flight)
+    # iteration's 2 LW loads may be in flight)
     events.setdefault(BARRIER_STEP, []).extend([f"s_waitcnt vmcnt({2 * LW})", "s_barrier"])
     # the iteration's scalar bookkeeping, spread over its last steps (after
-    # every load burst), then the exit test
+    # every load), then the exit test
     n = NQ + NP
     events.setdefault(n - 4, []).extend(desc_advance(S_KD))
     events.setdefault(n - 3, []).extend(desc_advance(S_VD))
     events.setdefault(n - 2, []).extend([f"s_add_u32 {s_(S_I)}, {s_(S_I)}, 1"])
     g.lines += stream(steps, nxt_steps, valu, events, LA, pre)
-    g.lines += [f"s_cmp_eq_u32 {s_(S_I)}, {s_(S_NTM1)}",
-                f"s_cbranch_scc1 {g.label(f'Llast{(u + 1) % 4}')}"]
+    if tests:
+        g.lines += [f"s_cmp_eq_u32 {s_(S_I)}, {s_(S_NTM1)}",
+                    f"s_cbranch_scc1 {g.label(f'Llast{(u + 1) % 4}')}"]
 
 
 def last_iteration(g, u):
@@ -508,7 +527,7 @@ def prologue(g):
            f"s_cselect_b32 {s_(S_MASKAT)}, -1, {s_(S_MASKAT)}"]
     # K_0, K_1, V_0, K_2, V_1
     for desc, ring, t in ((S_KD, KRING, 0), (S_KD, KRING, 1), (S_VD, VRING, 0), (S_KD, KRING, 2), (S_VD, VRING, 1)):
-        L_ += dma_tile(desc, ring, t) + desc_advance(desc)
+        L_ += sum(dma_tile(desc, ring, t), []) + desc_advance(desc)
     # Q^T fragments: 16 bytes per lane per (query block, k-step), into v0-v63
     for qb in range(2):
         for s in range(KS):
@@ -532,15 +551,36 @@ def prologue(g):
         L_ += tile0_max()
     L_ += sm_ops(0, 0, 0, True) + sm_ops(0, 0, 1, True)
     L_ += [f"s_cmp_eq_u32 {s_(S_NT)}, 1", f"s_cbranch_scc1 {g.label('Llast0')}"]
+    # the last iteration a block of four may run: n-2, or n-3 when the last
+    # tile is partial (iteration n-2 masks it); the first block runs if
+    # iterations 0..3 fit below it
+    L_ += [f"s_sub_i32 {s_(S_LIM)}, {s_(S_NT)}, 2",
+           f"s_and_b32 {s_(S_TMP)}, {s_(S_KVLEN)}, 63",
+           f"s_cmp_lg_u32 {s_(S_TMP)}, 0",
+           f"s_cselect_b32 {s_(S_TMP)}, 1, 0",
+           f"s_sub_i32 {s_(S_LIM)}, {s_(S_LIM)}, {s_(S_TMP)}",
+           f"s_cmp_ge_i32 {s_(S_LIM)}, 3",
+           f"s_cbranch_scc0 {g.label('Ltail')}"]
 
 
 def generate(fast=False):
     g = Gen(fast)
     prologue(g)
+    # blocks of four steady iterations i..i+3 while i + 3 <= S_LIM
     g.lines += [f"{g.label('Lloop')}:"]
     for u in range(4):
+        iteration(g, u, tests=False)
+    g.lines += [f"s_add_u32 {s_(S_TMP)}, {s_(S_I)}, 3",
+                f"s_cmp_le_i32 {s_(S_TMP)}, {s_(S_LIM)}",
+                f"s_cbranch_scc1 {g.label('Lloop')}",
+                f"s_cmp_eq_u32 {s_(S_I)}, {s_(S_NTM1)}",
+                f"s_cbranch_scc1 {g.label('Llast0')}"]
+    # the remaining steady iterations (at most four), each with the exit
+    # test and the mask of a partial last tile
+    g.lines += [f"{g.label('Ltail')}:"]
+    for u in range(4):
         iteration(g, u)
-    g.lines += [f"s_branch {g.label('Lloop')}"]
+    g.lines += [f"s_branch {g.label('Ltail')}"]
     for u in range(4):
         last_iteration(g, u)
     for par in range(2):

@@ -43,7 +43,7 @@ def test_fast_form_differs_from_the_checked_one_only_in_the_maximum(d):
     checked, fast = g.generate(), g.generate(fast=True)
     assert not any(x.startswith("v_cmp_nle") for x in fast)
     assert not any("Lslow" in x for x in fast)
-    assert sum(1 for x in checked if x.startswith("v_cmp_nle")) == 2 * 8   # 4 steady + 4 last iterations
+    assert sum(1 for x in checked if x.startswith("v_cmp_nle")) == 2 * 12   # 4 block + 4 tail + 4 last iterations
     keep = ("v_mfma", "ds_read", "buffer_load", "global_load", "s_waitcnt", "s_barrier")
     pick = lambda lines: [x for x in lines if x.startswith(keep)]
     assert pick(fast) == pick(checked)
@@ -69,10 +69,11 @@ def test_generated_loop_passes_its_checks(d, fast):
     assert g.check_hazards(lines) == []
     assert g.check_fragments(lines) == []
     mfma = [x for x in lines if x.startswith("v_mfma")]
-    # scores of tile 0, four unrolled iterations, four last iterations:
-    # 2 MFMAs per fragment step; D/8 score steps and D/8 P V steps per tile
+    # scores of tile 0, the block of four iterations, the four iterations of
+    # the tail loop, four last iterations: 2 MFMAs per fragment step; D/8
+    # score steps and D/8 P V steps per tile
     steps = d // 8
-    assert len(mfma) == 2 * (steps + 4 * 2 * steps + 4 * steps)
+    assert len(mfma) == 2 * (steps + 2 * 4 * 2 * steps + 4 * steps)
     # every scalar register the block writes is declared scratch or is a pinned in/out operand
     written = set()
     for x in lines:
