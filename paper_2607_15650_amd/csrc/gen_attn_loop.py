@@ -31,8 +31,14 @@ the hand schedule adds is register placement and instruction order:
   * the steady loop takes no branch but its loop-back: iterations run in
     blocks of four while none of the four is the last or masks a partial
     last tile, and the tests for those two run only in the few iterations
-    after the blocks; the slow path of the lazy maximum and the tail mask
-    are out of line.
+    after the blocks; the tail mask is out of line;
+  * two forms of the block: the checked one tests every tile's sums for the
+    lazy maximum and branches out of line into the slow path that raises
+    m; the fast one takes m from tile 0's scores in the prologue and never
+    raises it (no test, no branch per tile).  The kernel runs the fast form
+    and runs a task again in the checked form when a row sum ends above
+    2^40 or NaN; below that bound no tile of the checked form would have
+    raised m, so the two agree bit for bit.
 
 Register and LDS layout, the lazy running maximum and the accumulator layout
 of the 32x32x16 MFMA follow attn_bf16.hip.  Run `python gen_attn_loop.py`
