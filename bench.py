@@ -542,15 +542,28 @@ def sweep_result(w, steps, warmup):
         e1.record()
         torch.cuda.synchronize()
         ms = e0.elapsed_time(e1) / steps
+        # the attention call alone: events around it in a second pass
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for ea, eb in evs:
+            ea.record()
+            api.attn_partition_states(q, k, v, offs, mask, w.scale, st, ls, ws_k)
+            eb.record()
+            api.merge_states(st, ls, out, lse)
+            api.contrib(ls, lse, wp, ws)
+        torch.cuda.synchronize()
+        attn_ms = sum(ea.elapsed_time(eb) for ea, eb in evs) / steps
         flops = algorithmic(w, sel)[0]
         rows.append({"k": len(sel), "fraction": len(sel) / w.P, "ms_per_step": ms,
-                     "tflops": flops / (ms * 1e-3) / 1e12})
-        print(f"[bench] {w.name} k={len(sel)} {ms:.3f} ms", file=sys.stderr, flush=True)
-    ks = np.array([r["fraction"] for r in rows])
-    ts = np.array([r["ms_per_step"] for r in rows])
-    slope, icpt = np.polyfit(ks, ts, 1)
-    return {"workload": w.name, "steps": steps, "warmup": warmup, "points": rows,
-            "linear_fit_ms": {"slope_per_fraction": float(slope), "intercept": float(icpt)}}
+                     "tflops": flops / (ms * 1e-3) / 1e12, "attn_ms": attn_ms,
+                     "attn_frac_of_peak": flops / (attn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS})
+        print(f"[bench] {w.name} k={len(sel)} {ms:.3f} ms (attention {attn_ms:.3f} ms)", file=sys.stderr, flush=True)
+    res = {"workload": w.name, "steps": steps, "warmup": warmup, "points": rows}
+    if len(rows) > 1:
+        ks = np.array([r["fraction"] for r in rows])
+        ts = np.array([r["ms_per_step"] for r in rows])
+        slope, icpt = np.polyfit(ks, ts, 1)
+        res["linear_fit_ms"] = {"slope_per_fraction": float(slope), "intercept": float(icpt)}
+    return res
 
 
 def sweep(args, w):
@@ -562,7 +575,7 @@ def sweep(args, w):
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "D": w.D, "S": w.S, "P": w.P,
                    "query_partition": w.q, "q_len": w.q_len},
-        "sweep": r["points"], "linear_fit_ms": r["linear_fit_ms"],
+        "sweep": r["points"], "linear_fit_ms": r.get("linear_fit_ms"),
     }
     print(json.dumps(res), flush=True)
 
@@ -831,11 +844,13 @@ def main():
 def other_workloads():
     """The other workloads of the hot path, measured in the same run: the
     long-context selection sweep (131,072 tokens, 24 heads, 16 partitions,
-    nearest-first fresh sets of 1, 2, 4, 8 and 16 partitions) and the
-    planner-driven run (75,600 tokens, 40 heads, all 8 query blocks over 10
-    steps, anchors at steps 0 and 5) at the specified weight threshold 0.05
-    and at the uniform level 1/8.  Reported beside the headline figure, not in
-    it."""
+    nearest-first fresh sets of 1, 2, 4, 8 and 16 partitions), the
+    HunyuanVideo-like head-dim-64 step (118,800 tokens, 48 heads, fresh
+    {2,3,4} of 8) and the planner-driven run (75,600 tokens, 40 heads, all 8
+    query blocks over 10 steps, anchors at steps 0 and 5) at the specified
+    weight threshold 0.05 and at the uniform level 1/8.  Reported beside the
+    headline figure, not in it."""
+    import dataclasses
     import gc
     import torch
     from fixtures import get_workload
@@ -845,6 +860,11 @@ def other_workloads():
     torch.cuda.empty_cache()
     print("[bench] other workloads: long-context sweep", file=sys.stderr, flush=True)
     out["longctx_sweep"] = sweep_result(get_workload("longctx_bf16_h24_d128_s131072_p16"), steps=5, warmup=2)
+    gc.collect()
+    torch.cuda.empty_cache()
+    print("[bench] other workloads: head dim 64", file=sys.stderr, flush=True)
+    wh = get_workload("hunyuan_bf16_h48_d64_s118800_p8")
+    out["hunyuan_d64"] = sweep_result(dataclasses.replace(wh, sweep=(wh.select,)), steps=10, warmup=2)
     gc.collect()
     torch.cuda.empty_cache()
     print("[bench] other workloads: planner-driven run", file=sys.stderr, flush=True)
