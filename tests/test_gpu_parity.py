@@ -227,6 +227,12 @@ EDGE = [
     # the same at D=64, with enough heads for four rounds of tasks (the
     # hand-scheduled D=64 kernel runs launches of at least four rounds)
     ("bf16", 64, 128, 300, [130, 192, 300, 321, 440, 513]),
+    # full last tiles of 5, 8, 9 and 12 key tiles: the steady iterations run
+    # in blocks of four while none of them is the last, so the loop leaves a
+    # block straight for the last iteration (5, 9), after one or two blocks
+    # and a tail of three (8, 12)
+    ("bf16", 128, 2, 300, [320, 512, 576, 768]),
+    ("bf16", 64, 128, 300, [320, 512, 576, 768]),
     ("bf16", 64, 128, 257, [64, 128, 63, 65]),
     ("bf16", 64, 4, 384, [96, 192, 95, 97]),    # 1.5 and 3 tiles of 64 keys, 1.5 query tiles
     ("bf16", 64, 1, 385, [288, 1, 383]),
