@@ -840,7 +840,6 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_asm_kernel(const AttnArgs a)
     const float sl2 = a.scale_log2;
     const uint32_t ntiles = (uint32_t)((kv_len + BN - 1) / BN);
     const uint32_t kvl = (uint32_t)kv_len;
-    const uint32_t wv = (uint32_t)wave;
     const uint32_t wlds = __builtin_amdgcn_readfirstlane(smem_lds + (uint32_t)wave * (LW * 1024u));
     const uint32_t tileb = __builtin_amdgcn_readfirstlane(row_bytes * BN);
     // Two forms of the key loop.  The fast one takes the running maximum m
@@ -880,7 +879,7 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_asm_kernel(const AttnArgs a)
                  "{v242}"(vaddr[0]), "{v243}"(vaddr[1]), "{v244}"(vaddr[2]), "{v245}"(vaddr[3]),                      \
                  "{v246}"(dmak[0]), "{v247}"(dmak[1]), "{v248}"(dmak[2]), "{v249}"(dmak[3]),                          \
                  "{v250}"(dmav[0]), "{v251}"(dmav[1]), "{v252}"(dmav[2]), "{v253}"(dmav[3]),                          \
-                 "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s43}"(wv), "{s44}"(wlds), "{s45}"(tileb)             \
+                 "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s44}"(wlds), "{s45}"(tileb)             \
                : DITANGO_D128_LOOP_CLOBBERS)
         if (pass == 0) {
           DITANGO_D128_CALL(DITANGO_D128_FAST_ASM);
@@ -897,7 +896,7 @@ __global__ __launch_bounds__(256, 1) void attn_bf16_asm_kernel(const AttnArgs a)
                : "{v234}"(kaddr[0]), "{v235}"(kaddr[1]), "{v236}"(kaddr[2]), "{v237}"(kaddr[3]),                      \
                  "{v238}"(vaddr[0]), "{v239}"(vaddr[1]), "{v240}"(dmak[0]), "{v241}"(dmak[1]),                        \
                  "{v242}"(dmav[0]), "{v243}"(dmav[1]),                                                                \
-                 "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s43}"(wv), "{s44}"(wlds), "{s45}"(tileb)             \
+                 "{s40}"(sl2), "{s41}"(ntiles), "{s42}"(kvl), "{s44}"(wlds), "{s45}"(tileb)             \
                : DITANGO_D64_LOOP_CLOBBERS)
         if (pass == 0) {
           DITANGO_D64_CALL(DITANGO_D64_FAST_ASM);

@@ -110,7 +110,7 @@ def Q(qb, s):                  # AGPR Q^T fragments
 
 
 # scalar registers: inputs pinned by the caller, then scratch
-S_SL2, S_NT, S_KVLEN, S_WAVE, S_WLDS, S_TILEB = 40, 41, 42, 43, 44, 45
+S_SL2, S_NT, S_KVLEN, S_WLDS, S_TILEB = 40, 41, 42, 44, 45
 S_KD, S_VD = 48, 52            # buffer descriptors (4 each)
 S_I, S_TMP, S_BIG, S_MASKAT, S_RET, S_CMP, S_NTM1, S_LIM = 56, 57, 58, 59, 60, 62, 64, 65
 SCRATCH_SGPRS = list(range(56, 66))
