@@ -39,11 +39,11 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # elementwise copy reads / writes 1 GiB), keyed by the build id (source and
 # compile options) of the kernel they were taken on; reported only while the
 # build id matches.
-ATTN_TRAFFIC = {"build_id": "b0c36175586a4958", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "queue",
+ATTN_TRAFFIC = {"build_id": "52e804dedfc86dd5", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "queue",
                 # the balanced attention kernel (mean of 5 launches: the order
                 # in which tasks are claimed moves the reads by up to 1 %); the
                 # counter reset moves about 1 KiB
-                "fetch_bytes": 764210.6 * 1024 * 2.0, "write_bytes": 287959.9 * 1024 * 1.0}
+                "fetch_bytes": 766106.5 * 1024 * 2.0, "write_bytes": 287960.6 * 1024 * 1.0}
 
 
 def parse():
@@ -103,7 +103,7 @@ def algorithmic(w, select):
 # rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_LDS_BANK_CONFLICT
 # (busy fraction = busy cycles / (1024 SIMDs x GRBM cycles / 8 XCDs); clock =
 # GRBM cycles / 8 / the traced kernel duration); reported under the same rule.
-ATTN_COUNTERS = {"mfma_busy": 0.840, "lds_bank_conflicts": 2269440, "clock_ghz": 1.61}
+ATTN_COUNTERS = {"mfma_busy": 0.851, "lds_bank_conflicts": 2269440, "clock_ghz": 1.56}
 
 
 # HBM bytes per launch of the merge kernel at the default workload (all P
