@@ -39,7 +39,7 @@ PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 # elementwise copy reads / writes 1 GiB), keyed by the build id (source and
 # compile options) of the kernel they were taken on; reported only while the
 # build id matches.
-ATTN_TRAFFIC = {"build_id": "52e804dedfc86dd5", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "queue",
+ATTN_TRAFFIC = {"build_id": "f6b4934c947b132e", "workload": "videodit_bf16_h40_d128_s75600_p8", "mode": "queue",
                 # the balanced attention kernel (mean of 5 launches: the order
                 # in which tasks are claimed moves the reads by up to 1 %); the
                 # counter reset moves about 1 KiB

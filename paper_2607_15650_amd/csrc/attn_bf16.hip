@@ -33,7 +33,21 @@
 //   K reads (16 consecutive keys, one unit) and the transpose reads of V
 //   (4 consecutive keys x 4 units) hit 16 distinct 16-byte bank groups.
 //
-// Pipeline
+// Two kernels
+//   Launches at D=128, and at D=64 when they run at least four rounds of
+//   tasks, use attn_bf16_asm_kernel: four waves, one per SIMD, two 32-row
+//   query blocks per wave so that every LDS fragment feeds two MFMAs, the
+//   O^T accumulators and Q^T in AGPRs, and a key loop written as gfx950
+//   assembly by gen_attn_loop.py (attn_d128_loop.inc, attn_d64_loop.inc).
+//   Its fast loop keeps tile 0's maximum for the whole task (no per-tile
+//   test); a workgroup whose row sums end above 2^40 or NaN runs its task
+//   again in the checked loop, which follows the running-maximum rule below
+//   and agrees with the fast loop bit for bit wherever the fast one is kept.
+//   The compiled kernel attn_bf16_kernel (the pipeline below) runs the
+//   other launches: short D=64 launches, and partitions whose bytes for one
+//   head reach the tile loads' 32-bit bounds.
+//
+// Pipeline of the compiled kernel
 //   D=128 (two waves per SIMD): iteration i computes the scores of tile i+1
 //   (MFMA) in the same basic block as the exponentials of tile i (VALU), then
 //   accumulates P_i V_i (MFMA).  The loads of K_{i+2} and V_{i+1} are in
