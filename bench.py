@@ -785,6 +785,11 @@ def main():
                 args.power_seconds),
             "mfma_probe": power_during(torch, lambda: api.probe_mfma_bf16(n_wg, 20000, sink), args.power_seconds),
         }
+        # the attention rate against the peak at the clock the card ran the
+        # attention launches at (the published peak assumes 2.4 GHz)
+        mhz = ref["power"]["attn_partition_states"].get("gfx_mhz_mean") if ref["power"]["attn_partition_states"] else None
+        if w.dtype == "bf16" and mhz:
+            ref["attn_frac_of_peak_at_sampled_clock"] = achieved / (PEAK_BF16_TFLOPS * mhz / 2400.0)
     del sink
 
     cpu = None
